@@ -1,0 +1,274 @@
+/*
+ * cap.h -- C ABI of the CAP expert-parallel MoE layer hot path on one MI355X.
+ *
+ * The library implements, as HIP kernels for gfx950, the per-GPU steps of an
+ * expert-parallel MoE layer under CAP ("Communication-Aware Placement and
+ * Pruning for Efficient Mixture-of-Experts Inference"):
+ *   top-k routing and normalised gates (Sec. II-A, Eq. 1);
+ *   communication-aware device-level pruning (Sec. VI, Eq. 6 and its greedy);
+ *   the device-centric all-to-all layout and send volume (Sec. II-C, Eq. 3);
+ *   token permutation; SwiGLU expert FFN over one rank's experts; the weighted
+ *   combine (Sec. II-C, Eq. 1); expert co-activation counts (Sec. IV-B).
+ * Expert-parallel ranks are virtual: all of them live on the one GPU.
+ *
+ * Conventions for every call
+ *   - Array arguments are DEVICE pointers unless stated otherwise; sizes are
+ *     host scalars.  The caller allocates and owns every buffer, including the
+ *     workspace; the library never allocates, frees or keeps a pointer after
+ *     the call returns (it only enqueues work).
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
+ *     is asynchronous on that stream and never synchronises with the host.
+ *   - Arguments are validated on the host before anything is launched; an
+ *     invalid call returns an error and enqueues nothing.  Errors of a launched
+ *     kernel surface at the caller's next synchronisation.
+ *   - Results are deterministic: the same inputs give bit-identical outputs.
+ *   - Calls on different streams with distinct output and workspace buffers
+ *     may run concurrently (the library keeps no state).
+ *   - Row-major layouts; "[A][B]" means A rows of B contiguous elements.
+ *
+ * Limits: 1 <= k <= 8, E <= 256, R <= 64 (device masks are uint64), E % R == 0,
+ * T % R == 0, T*k < 2^31.  bf16 is stored as raw 16-bit patterns.
+ */
+#ifndef CAP_H
+#define CAP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CAP_OK = 0,
+    CAP_ERR_INVALID_ARG = -1,  /* null pointer, bad size, bad limit */
+    CAP_ERR_UNSUPPORTED = -2,  /* dtype / mode / shape combination not built */
+    CAP_ERR_WORKSPACE = -3,    /* workspace too small */
+    CAP_ERR_HIP = -4           /* a kernel launch failed */
+} cap_status;
+
+typedef enum { CAP_DTYPE_F32 = 0, CAP_DTYPE_BF16 = 1 } cap_dtype;
+
+typedef enum {
+    /* destination side: the expanded, expert-sorted rows one rank computes on
+       (pack + all-to-all + expand collapsed into one gather on one GPU) */
+    CAP_PERMUTE_EXPERT_GATHER = 0,
+    /* source side: the rank's send buffer, one row per (token, kept device) */
+    CAP_PERMUTE_SEND_PACK = 1
+} cap_permute_mode;
+
+typedef enum {
+    CAP_COMBINE_DEST_REDUCE = 0, /* per received token: weighted sum of the rank's expert rows */
+    CAP_COMBINE_SRC_REDUCE = 1   /* per source token: sum of the returned rows (+ shared) */
+} cap_combine_mode;
+
+typedef enum {
+    CAP_OP_ROUTE_PRUNE = 0,
+    CAP_OP_DISPATCH_LAYOUT = 1,
+    CAP_OP_PERMUTE = 2,
+    CAP_OP_EXPERT_FFN = 3,
+    CAP_OP_COMBINE = 4,
+    CAP_OP_COACTIVATION = 5
+} cap_op;
+
+/*
+ * Expert-parallel topology and placement (Sec. IV-B: placement pi maps expert
+ * -> GPU; node(.) maps GPU -> node; Eq. 3 costs 0 / 1 / c).
+ *   T tokens in total; token t belongs to source rank t / tokens_per_rank
+ *   (each rank runs its own requests, Sec. I); rank r is on node
+ *   r / ranks_per_node.  Every rank holds E_loc = E / R experts.
+ *   expert_rank[e]  (device, [E]) rank holding expert e;
+ *   expert_local[e] (device, [E]) slot of expert e within its rank, in [0, E_loc);
+ *                   (expert_rank, expert_local) must be a bijection onto
+ *                   [0,R) x [0,E_loc).  Out-of-range entries are ignored by the
+ *                   kernels (no write happens for them) and give meaningless
+ *                   output, never an out-of-bounds access.
+ *   inter_node_cost c >= 1: pruning cost of a device on another node; a device
+ *                   on the same node costs 1 and the token's own device 0.
+ * The "slot position" of expert e is P(e) = expert_rank[e]*E_loc + expert_local[e].
+ */
+typedef struct {
+    int32_t E;
+    int32_t R;
+    int32_t ranks_per_node;
+    int32_t T;
+    int32_t tokens_per_rank;
+    int32_t k;
+    const int32_t *expert_rank;
+    const int32_t *expert_local;
+    float inter_node_cost;
+} cap_topology;
+
+/*
+ * Outputs of cap_dispatch_layout, inputs of the later steps (all device).
+ *   send_counts[R][R]   tokens of source s sent to device d (d == s counted):
+ *                       one copy per (token, kept device), Sec. II-C.
+ *   send_offsets[R][R]  exclusive scan of send_counts over d within s: row of
+ *                       the first token for d in s's send buffer.
+ *   recv_offsets[R+1]   exclusive scan over d of U_d = sum_s send_counts[s][d];
+ *                       U_d rows form device d's receive buffer (tokens
+ *                       ascending, i.e. source-major) and the buffers of all
+ *                       devices are concatenated in device order.
+ *   recv_token[T*k]     recv_token[recv_offsets[d] + u] = token of row u of d's
+ *                       receive buffer (first recv_offsets[R] entries written).
+ *   expert_counts[E]    kept (token, expert) pairs per expert, by slot position.
+ *   expert_offsets[E+1] exclusive scan of expert_counts in slot-position order:
+ *                       rank r's expert-sorted rows are
+ *                       [expert_offsets[r*E_loc], expert_offsets[(r+1)*E_loc]).
+ *   slot_pos[T][k]      row of kept slot (t,s) in that concatenation (tokens
+ *                       ascending within an expert); -1 if pruned.
+ *   copy_row[T][k]      row of token t in the receive buffer of the device of
+ *                       slot s; -1 if pruned.  Slots on one device share it.
+ *   vol[T][4]           per token: n_dev (kept devices, own included),
+ *                       n_intra_remote (other devices of the own node),
+ *                       n_inter (devices on other nodes), n_nodes.
+ *   totals[4]           int64 sums of vol over all tokens.
+ */
+typedef struct {
+    int32_t *send_counts;
+    int32_t *send_offsets;
+    int32_t *recv_offsets;
+    int32_t *recv_token;
+    int32_t *expert_counts;
+    int32_t *expert_offsets;
+    int32_t *slot_pos;
+    int32_t *copy_row;
+    uint8_t *vol;
+    int64_t *totals;
+} cap_layout;
+
+/* Human-readable name of a status code (static string; never NULL). */
+const char *cap_status_string(cap_status s);
+
+/* Library version: major*10000 + minor*100 + patch. */
+int32_t cap_version(void);
+
+/*
+ * Workspace bytes that `op` needs for this topology and shape (0 if none).
+ *   CAP_OP_DISPATCH_LAYOUT: per-chunk partial counts (uses topo only).
+ *   CAP_OP_EXPERT_FFN: the SwiGLU intermediate H, max_rows x inter values of
+ *                      `dtype` (topo and d unused, may be NULL / 0).
+ *   CAP_OP_COACTIVATION: per-split partial counts (uses topo->T and topo->E).
+ *   Other ops need none.
+ * Returns 0 for invalid arguments as well.
+ */
+size_t cap_workspace_size(cap_op op, const cap_topology *topo, int32_t d, int32_t inter,
+                          int32_t max_rows, cap_dtype dtype);
+
+/*
+ * Top-k routing, normalised gates and communication-aware pruning, for all T
+ * tokens (Eq. 1; Sec. VI, Eq. 6 and the greedy that follows it).
+ *   logits[T][E] fp32 router logits (finite; non-finite input is a
+ *                precondition violation with unspecified output).
+ *   p            pruning threshold, 0 <= p < 1 (fp32).  p == 0 keeps every slot.
+ * Outputs:
+ *   idx[T][k]    experts in slot order: descending logit, equal logits by lower
+ *                expert index (-0.0 == +0.0).
+ *   w[T][k]      pruned, renormalised gates: w_s = q_s / S with
+ *                q_s = cap_exp(logit_s - logit_0) and S their fp32 sum in slot
+ *                order; a device d gets a_d = sum of w_s on d (slot order);
+ *                devices are kept in descending a_d / cost_d (own device first,
+ *                ties by lower id) until the fp32 running sum >= 1 - p; then
+ *                w'_s = w_s / S' (S' = fp32 sum of kept w_s in slot order), 0
+ *                for pruned slots.  cap_exp is the Cody-Waite reduced,
+ *                degree-7 Taylor exponential in fp32 with fmaf (0 below -87.33).
+ *   keep[T][k]   1 if the slot's device is kept, else 0.
+ *   dst_mask[T]  bit d set for every kept device.
+ * No workspace.
+ */
+cap_status cap_route_prune(const cap_topology *topo, const float *logits, float p,
+                           int32_t *idx, float *w, uint8_t *keep, uint64_t *dst_mask,
+                           void *stream);
+
+/*
+ * Counting and prefix scans into the all-to-all send layout, the expert-sorted
+ * layout and per-token send volume (Sec. II-C device-centric transfer; Eq. 3
+ * topology classes).  Inputs: the outputs of cap_route_prune.  Outputs: every
+ * array of `out` (see cap_layout).  Needs cap_workspace_size(CAP_OP_DISPATCH_LAYOUT).
+ */
+cap_status cap_dispatch_layout(const cap_topology *topo, const int32_t *idx, const uint8_t *keep,
+                               const uint64_t *dst_mask, const cap_layout *out,
+                               void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Token permutation, rows of d values of `dtype` (d % 8 == 0 for bf16, % 4 for f32).
+ *   CAP_PERMUTE_EXPERT_GATHER, rank r: out[slot_pos(t,s) - expert_offsets[r*E_loc]]
+ *       = x[t] for every kept slot on r.  out holds rank r's expert-sorted rows.
+ *   CAP_PERMUTE_SEND_PACK, rank s: out[send_offsets[s][d] + j] = x[t] for the
+ *       j-th token t of s (ascending) whose mask holds d.
+ * x is [T][d].  The layout arrays come from cap_dispatch_layout.
+ * out_rows is the capacity of `out` in rows: rows at or past it are not
+ * written (size it with expert_offsets / send_counts, or an upper bound such
+ * as T*min(k, E_loc) for EXPERT_GATHER and T_loc*min(k, R) for SEND_PACK).
+ */
+cap_status cap_permute(const cap_topology *topo, cap_permute_mode mode, int32_t rank,
+                       cap_dtype dtype, int32_t d, const void *x,
+                       const int32_t *idx, const uint8_t *keep, const uint64_t *dst_mask,
+                       const cap_layout *lay, void *out, int32_t out_rows, void *stream);
+
+/*
+ * SwiGLU expert FFN over one rank's experts (Eq. 1 Expert_i; SwiGLU experts):
+ *   for local expert l and each of its rows x:
+ *   y = W2_l (silu(W1_l x) * (W3_l x)),  silu(z) = z / (1 + e^-z).
+ *   xs[.][d]          expert-sorted input rows; expert l owns rows
+ *                     [row_offsets[l] - row_offsets[0], row_offsets[l+1] - row_offsets[0]).
+ *   row_offsets[E_loc+1] (device) non-decreasing row offsets (e.g. the rank's
+ *                     slice of expert_offsets); read on the device, so the host
+ *                     never needs the counts.
+ *   max_rows          capacity of xs, y and the workspace, in rows.  Rows past
+ *                     max_rows are not computed.
+ *   w1, w3 [E_loc][inter][d]; w2 [E_loc][d][inter] (K-contiguous rows).
+ *   y[.][d]           output rows, same row order as xs.
+ * bf16: fp32 accumulation, H rounded to bf16 between the two GEMMs, y bf16;
+ *       needs d % 256 == 0 and inter % 128 == 0.
+ * f32:  fp32 throughout; needs d % 4 == 0.
+ * Shared experts: call with E_loc = 1, row_offsets = {0, n}, inter = the
+ * concatenated intermediate size.  Workspace: cap_workspace_size(CAP_OP_EXPERT_FFN).
+ */
+cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter,
+                          int32_t max_rows, const void *xs, const int32_t *row_offsets,
+                          const void *w1, const void *w3, const void *w2, void *y,
+                          void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Weighted combine (Sec. II-C local aggregation and final combination; Eq. 1).
+ *   CAP_COMBINE_DEST_REDUCE, rank r: in = rank r's expert output rows (row order
+ *       of CAP_PERMUTE_EXPERT_GATHER); for each row u < U_r of r's receive buffer,
+ *       token t = recv_token[recv_offsets[r] + u]:
+ *       out[recv_offsets[r] + u] = sum over kept slots s of t placed on r of
+ *       w'_s * in[slot_pos(t,s) - expert_offsets[r*E_loc]].
+ *       `out` is the concatenated receive-side buffer of all ranks.
+ *   CAP_COMBINE_SRC_REDUCE, rank s: in = that concatenated buffer (the rows each
+ *       device returns); for each token t of s:
+ *       out[t - s*tokens_per_rank] = sum over kept devices d of t (ascending) of
+ *       in[recv_offsets[d] + copy_row(t,d)]  (+ shared_out[t - s*tokens_per_rank]
+ *       if shared_out != NULL).
+ * fp32 accumulation; rows of d values of `dtype` (d % 8 == 0 for bf16, % 4 for f32).
+ * in_rows / out_rows are the capacities of `in` / `out` in rows: rows at or past
+ * them are neither read (their contribution is skipped) nor written.
+ * SRC_REDUCE needs out_rows >= tokens_per_rank.
+ */
+cap_status cap_combine(const cap_topology *topo, cap_combine_mode mode, int32_t rank,
+                       cap_dtype dtype, int32_t d, const void *in, int32_t in_rows,
+                       const int32_t *idx, const float *w, const uint8_t *keep,
+                       const uint64_t *dst_mask, const cap_layout *lay,
+                       const void *shared_out, void *out, int32_t out_rows, void *stream);
+
+/*
+ * Expert co-activation counts on the (pruned) routing (Sec. IV-B; placement
+ * runs on pruned traces, Sec. VII):
+ *   coact[i][j] (i != j) = tokens that keep both i and j; coact[i][i] = tokens
+ *   that keep i.  accumulate != 0 adds to coact (trace windows), else overwrites.
+ * idx/keep are [T][k] as produced by cap_route_prune (out-of-range experts are
+ * skipped).  Workspace: cap_workspace_size(CAP_OP_COACTIVATION, topo with this T and E, ...);
+ * 16-byte aligned.
+ */
+cap_status cap_coactivation(int32_t T, int32_t k, int32_t E, const int32_t *idx,
+                            const uint8_t *keep, uint32_t *coact, int32_t accumulate,
+                            void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAP_H */

@@ -1,0 +1,182 @@
+"""One expert-parallel MoE layer step on one GPU with virtual ranks.
+
+Owns the device buffers (torch) and chains the C-ABI calls in the order of the
+layer (Sec. II-B/II-C; Sec. VI):
+
+  route_prune (all T tokens)  -> dispatch_layout -> coactivation
+  expert_gather(rank) -> expert_ffn(rank) -> dest_reduce(rank)
+  [shared experts on the source rank's tokens] -> src_reduce(rank)
+
+Every step runs in libcap.so's HIP kernels; this module only allocates and
+passes pointers.  All calls are asynchronous on the current stream.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import capi
+
+_BF16 = torch.bfloat16
+
+
+def to_device_rows(a: np.ndarray, dtype: str, device) -> torch.Tensor:
+    """numpy rows (uint16 bf16 bits or float32) -> device tensor of that storage type."""
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(_BF16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+
+class DeviceLayer:
+    """Buffers and calls for one layer configuration.
+
+    cfg: workloads.generator.Config (shapes only).  logits / x are numpy arrays
+    (x as uint16 bf16 bits for bf16 configs).  expert_rank / expert_local: int32
+    numpy [E].  row_cap: rows allocated per rank for expert rows (None = the
+    T*min(k, E_loc) bound).
+    """
+
+    def __init__(self, cfg, logits: np.ndarray, x: np.ndarray, expert_rank, expert_local, p: float,
+                 c: float = 5.0, device: str = "cuda", row_cap: int | None = None,
+                 recv_cap: int | None = None):
+        self.cfg = cfg
+        self.dev = torch.device(device)
+        self.p = float(p)
+        self.dt = capi.CAP_DTYPE_BF16 if cfg.dtype == "bf16" else capi.CAP_DTYPE_F32
+        self.tdt = _BF16 if cfg.dtype == "bf16" else torch.float32
+        T, E, k, R = cfg.T, cfg.E, cfg.k, cfg.R
+        d = self.d = cfg.d
+        i32 = dict(dtype=torch.int32, device=self.dev)
+        self.expert_rank = torch.as_tensor(np.asarray(expert_rank, np.int32)).to(self.dev)
+        self.expert_local = torch.as_tensor(np.asarray(expert_local, np.int32)).to(self.dev)
+        self.topo = capi.make_topology(E, R, cfg.ranks_per_node, T, k, self.expert_rank,
+                                       self.expert_local, c)
+        self.logits = torch.from_numpy(np.ascontiguousarray(logits, np.float32)).to(self.dev)
+        self.x = to_device_rows(x, cfg.dtype, self.dev)
+        # routing
+        self.idx = torch.empty((T, k), **i32)
+        self.w = torch.empty((T, k), dtype=torch.float32, device=self.dev)
+        self.keep = torch.empty((T, k), dtype=torch.uint8, device=self.dev)
+        self.mask = torch.empty(T, dtype=torch.int64, device=self.dev)
+        # layout
+        self.lay_t = dict(
+            send_counts=torch.empty((R, R), **i32), send_offsets=torch.empty((R, R), **i32),
+            recv_offsets=torch.empty(R + 1, **i32), recv_token=torch.empty(T * k, **i32),
+            expert_counts=torch.empty(E, **i32), expert_offsets=torch.empty(E + 1, **i32),
+            slot_pos=torch.empty((T, k), **i32), copy_row=torch.empty((T, k), **i32),
+            vol=torch.empty((T, 4), dtype=torch.uint8, device=self.dev),
+            totals=torch.empty(4, dtype=torch.int64, device=self.dev))
+        self.lay = capi.make_layout(self.lay_t)
+        self.ws_layout = self._ws(capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, self.topo))
+        self.coact = torch.zeros((E, E), dtype=torch.int32, device=self.dev)
+        self.ws_coact = self._ws(capi.cap_workspace_size(capi.CAP_OP_COACTIVATION, self.topo))
+        # rank-side buffers
+        self.row_cap = row_cap if row_cap is not None else T * min(k, cfg.E_loc)
+        self.recv_cap = recv_cap if recv_cap is not None else T * min(k, R)
+        self.xs = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
+        self.Y = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
+        self.parts = torch.zeros((self.recv_cap, d), dtype=self.tdt, device=self.dev)
+        self.y = torch.empty((cfg.tokens_per_rank, d), dtype=self.tdt, device=self.dev)
+        self.ws_ffn = self._ws(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, cfg.inter,
+                                                       self.row_cap, self.dt))
+        self.weights: dict[int, tuple] = {}
+        self.shared = None
+        self.shared_out = None
+        self.ws_shared = None
+
+    def _ws(self, nbytes: int) -> torch.Tensor:
+        # 256-byte aligned by the caching allocator
+        return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=self.dev)
+
+    # ------------------------------------------------------------ weights
+    def set_rank_weights(self, rank: int, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray):
+        """w1, w3 [E_loc][inter][d], w2 [E_loc][d][inter] in local-slot order (storage type)."""
+        self.weights[rank] = tuple(to_device_rows(w, self.cfg.dtype, self.dev) for w in (w1, w3, w2))
+
+    def set_shared_weights(self, w1, w3, w2):
+        self.shared = tuple(to_device_rows(w, self.cfg.dtype, self.dev) for w in (w1, w3, w2))
+        inter = self.shared[0].shape[0]
+        T_loc = self.cfg.tokens_per_rank
+        self.shared_out = torch.empty((T_loc, self.d), dtype=self.tdt, device=self.dev)
+        self.ws_shared = self._ws(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, self.d, inter,
+                                                          T_loc, self.dt))
+        self.shared_offsets = torch.tensor([0, T_loc], dtype=torch.int32, device=self.dev)
+
+    # ------------------------------------------------------------ steps
+    def route(self, stream=None):
+        capi.cap_route_prune(self.topo, self.logits, self.p, self.idx, self.w, self.keep, self.mask, stream)
+
+    def layout(self, stream=None):
+        capi.cap_dispatch_layout(self.topo, self.idx, self.keep, self.mask, self.lay, self.ws_layout,
+                                 stream=stream)
+
+    def coactivation(self, accumulate=False, stream=None):
+        capi.cap_coactivation(self.cfg.T, self.cfg.k, self.cfg.E, self.idx, self.keep, self.coact,
+                              accumulate, self.ws_coact, stream=stream)
+
+    def gather(self, rank: int, stream=None):
+        capi.cap_permute(self.topo, capi.CAP_PERMUTE_EXPERT_GATHER, rank, self.dt, self.d, self.x,
+                         self.idx, self.keep, self.mask, self.lay, self.xs, self.row_cap, stream)
+
+    def send_pack(self, rank: int, out: torch.Tensor, stream=None):
+        capi.cap_permute(self.topo, capi.CAP_PERMUTE_SEND_PACK, rank, self.dt, self.d, self.x,
+                         self.idx, self.keep, self.mask, self.lay, out, out.shape[0], stream)
+
+    def ffn(self, rank: int, stream=None):
+        w1, w3, w2 = self.weights[rank]
+        E_loc = self.cfg.E_loc
+        offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
+        capi.cap_expert_ffn(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.xs, offs,
+                            w1, w3, w2, self.Y, self.ws_ffn, stream=stream)
+
+    def shared_ffn(self, rank: int, stream=None):
+        if self.shared is None:
+            return
+        w1, w3, w2 = self.shared
+        T_loc = self.cfg.tokens_per_rank
+        xs = self.x[rank * T_loc:(rank + 1) * T_loc]
+        capi.cap_expert_ffn(self.dt, 1, self.d, w1.shape[0], T_loc, xs, self.shared_offsets,
+                            w1, w3, w2, self.shared_out, self.ws_shared, stream=stream)
+
+    def dest_reduce(self, rank: int, stream=None):
+        capi.cap_combine(self.topo, capi.CAP_COMBINE_DEST_REDUCE, rank, self.dt, self.d, self.Y,
+                         self.row_cap, self.idx, self.w, self.keep, self.mask, self.lay, None,
+                         self.parts, self.recv_cap, stream)
+
+    def src_reduce(self, rank: int, stream=None):
+        capi.cap_combine(self.topo, capi.CAP_COMBINE_SRC_REDUCE, rank, self.dt, self.d, self.parts,
+                         self.recv_cap, self.idx, self.w, self.keep, self.mask, self.lay,
+                         self.shared_out if self.shared is not None else None, self.y,
+                         self.y.shape[0], stream)
+
+    def front(self, stream=None):
+        """Routing front end over all virtual ranks' tokens."""
+        self.route(stream)
+        self.layout(stream)
+        self.coactivation(False, stream)
+
+    def rank_path(self, rank: int, stream=None):
+        """The destination and source work of one rank."""
+        self.gather(rank, stream)
+        self.ffn(rank, stream)
+        self.dest_reduce(rank, stream)
+        self.shared_ffn(rank, stream)
+        self.src_reduce(rank, stream)
+
+    def step(self, rank: int = 0, stream=None):
+        self.front(stream)
+        self.rank_path(rank, stream)
+
+    # ------------------------------------------------------------ host views
+    def host(self, name: str) -> np.ndarray:
+        if name in self.lay_t:
+            return self.lay_t[name].cpu().numpy()
+        t = getattr(self, name)
+        if t.dtype == _BF16:
+            return t.view(torch.int16).cpu().numpy().view(np.uint16)
+        return t.cpu().numpy()
+
+    def rank_rows(self, rank: int) -> int:
+        eo = self.lay_t["expert_offsets"].cpu().numpy()
+        E_loc = self.cfg.E_loc
+        return int(eo[(rank + 1) * E_loc] - eo[rank * E_loc])

@@ -1,0 +1,295 @@
+"""GPU parity: every C-ABI call against the CPU oracle on the same seeded inputs.
+
+Bit-exact: routing indices, gates, keep masks, device masks, every layout
+array, volumes, co-activation counts, permuted rows.  FFN and combine:
+|gpu - ref| <= 1e-3 + 2e-2 |ref| element-wise against the fp64 oracle, plus a
+normalised Frobenius error gate (1e-2 bf16, 1e-5 fp32).
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from tests import cases as C
+from workloads import generator as gen
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+from paper_2607_05116_amd import capi  # noqa: E402
+from paper_2607_05116_amd.layer import DeviceLayer  # noqa: E402
+
+import oracle  # noqa: E402
+
+
+def _layer(case: C.Case, x=None, **kw) -> DeviceLayer:
+    """Device layer of a case; without x, a narrow dummy activation (routing-only tests)."""
+    cfg = case.cfg
+    er, el = C.placement(case.name, case.placement, case.p, case.c)
+    if x is None:
+        dd = 8 if cfg.dtype == "bf16" else 4
+        x = np.zeros((cfg.T, dd), np.uint16 if cfg.dtype == "bf16" else np.float32)
+        cfg = dataclasses.replace(cfg, d=dd)
+    return DeviceLayer(cfg, C.logits(case.name), x, er, el, case.p, case.c, **kw)
+
+
+@pytest.mark.parametrize("case", C.ROUTE_CASES, ids=lambda c: c.id)
+def test_route_layout_coact_bit_exact(case):
+    L = _layer(case, row_cap=8, recv_cap=8)
+    L.front()
+    torch.cuda.synchronize()
+    r, lay = C.oracle_routing(case.name, case.placement, case.p, case.c)
+    assert np.array_equal(L.host("idx"), r["idx"])
+    assert np.array_equal(L.host("w").view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(L.host("keep"), r["keep"])
+    assert np.array_equal(L.host("mask").view(np.uint64), r["mask"])
+    for name in ("send_counts", "send_offsets", "recv_offsets", "expert_counts", "expert_offsets",
+                 "slot_pos", "copy_row", "vol", "totals"):
+        assert np.array_equal(L.host(name), lay[name]), name
+    n_recv = int(lay["recv_offsets"][-1])
+    assert np.array_equal(L.host("recv_token")[:n_recv], lay["recv_token"])
+    coact = oracle.coactivation(r["idx"], r["keep"], case.cfg.E)
+    assert np.array_equal(L.host("coact").view(np.uint32), coact)
+
+
+def test_coactivation_accumulate():
+    case = C.ROUTE_CASES[3]
+    L = _layer(case, row_cap=8, recv_cap=8)
+    L.route()
+    L.coactivation(False)
+    L.coactivation(True)
+    torch.cuda.synchronize()
+    r, _ = C.oracle_routing(case.name, case.placement, case.p, case.c)
+    coact = oracle.coactivation(r["idx"], r["keep"], case.cfg.E)
+    assert np.array_equal(L.host("coact").view(np.uint32), 2 * coact)
+
+
+def _adversarial_logits(T, E, seed):
+    rng = np.random.default_rng(seed)
+    L = rng.standard_normal((T, E)).astype(np.float32)
+    L[: T // 4] = gen.bf16_bits_to_f32(gen.f32_to_bf16_bits(L[: T // 4] * 0.02))  # heavy ties
+    L[T // 4: T // 4 + 8] = 0.0                                                    # all equal
+    L[T // 4 + 8: T // 4 + 16] = -0.0
+    L[T // 4 + 16: T // 4 + 24, ::2] = -0.0                                        # +-0 mix
+    return L
+
+
+@pytest.mark.parametrize("E,k,R,rpn,p,c", [
+    (16, 2, 4, 4, 0.3, 5.0), (64, 6, 8, 4, 0.25, 5.0), (128, 8, 16, 8, 0.1, 5.0),
+    (256, 8, 32, 8, 0.2, 3.0), (7, 3, 1, 1, 0.4, 5.0), (24, 5, 6, 2, 0.5, 2.0),
+    (128, 8, 64, 8, 0.3, 5.0), (96, 1, 8, 8, 0.0, 5.0), (40, 8, 4, 2, 0.05, 5.0)])
+def test_route_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
+    T = R * 160
+    L = _adversarial_logits(T, E, E + k)
+    perm = np.random.default_rng(R).permutation(E)
+    er, el = (perm // (E // R)).astype(np.int32), (perm % (E // R)).astype(np.int32)
+    cfg = gen.Config("adv", T=T, d=8, E=E, k=k, inter=128, R=R, ranks_per_node=rpn, n_clusters=1,
+                     zipf_s=0.0, dtype="bf16")
+    Ld = DeviceLayer(cfg, L, np.zeros((T, 8), np.uint16), er, el, p, c, row_cap=8, recv_cap=8)
+    Ld.front()
+    torch.cuda.synchronize()
+    r = oracle.route_prune(L, k, er, rpn, T // R, c, p)
+    lay = oracle.dispatch_layout(r["idx"], r["keep"], r["mask"], er, el, R, rpn, T // R, E)
+    assert np.array_equal(Ld.host("idx"), r["idx"])
+    assert np.array_equal(Ld.host("w").view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(Ld.host("mask").view(np.uint64), r["mask"])
+    for name in ("slot_pos", "copy_row", "vol", "expert_offsets", "send_counts", "totals"):
+        assert np.array_equal(Ld.host(name), lay[name]), name
+    assert np.array_equal(Ld.host("coact").view(np.uint32), oracle.coactivation(r["idx"], r["keep"], E))
+
+
+def test_determinism_front_end():
+    case = C.ROUTE_CASES[5]
+    L = _layer(case, row_cap=8, recv_cap=8)
+    outs = []
+    for _ in range(3):
+        L.front()
+        torch.cuda.synchronize()
+        outs.append([L.host(n).copy() for n in ("idx", "w", "keep", "mask", "slot_pos", "copy_row", "coact")])
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+    for a, b in zip(outs[0], outs[2]):
+        assert np.array_equal(a, b)
+
+
+# ---------------------------------------------------------------- permutation
+@pytest.mark.parametrize("name,kind,p", [("c1", "seq", 0.3), ("c2", "coact", 0.3)])
+def test_permute_exact(name, kind, p):
+    case = C.Case(name, gen.CONFIGS[name], kind, p)
+    cfg = case.cfg
+    x = gen.activations(cfg)
+    L = _layer(case, x=x)
+    L.front()
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    er, _ = C.placement(name, kind, p, 5.0)
+    ranks = range(cfg.R) if cfg.R <= 4 else [0, cfg.R - 1]
+    for rank in ranks:
+        L.gather(rank)
+        torch.cuda.synchronize()
+        want = oracle.expert_gather(x, r["idx"], r["keep"], lay["slot_pos"], lay["expert_offsets"], er, cfg.R, rank)
+        got = L.host("xs")[: want.shape[0]]
+        assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), rank
+        out = torch.empty((int(lay["send_counts"][rank].sum()), cfg.d), dtype=L.tdt, device="cuda")
+        L.send_pack(rank, out)
+        torch.cuda.synchronize()
+        want = oracle.send_pack(x, r["mask"], lay["send_offsets"], lay["send_counts"], cfg.R,
+                                cfg.tokens_per_rank, rank)
+        got = out.view(torch.int16).cpu().numpy() if cfg.dtype == "bf16" else out.cpu().numpy()
+        assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), rank
+
+
+# ---------------------------------------------------------------- expert FFN
+def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0):
+    """cap_expert_ffn on synthetic ragged experts; returns (gpu Y, oracle Y)."""
+    rng = np.random.default_rng(seed)
+    rows = int(sum(counts))
+    offs = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32) + 17    # non-zero base
+    x32 = rng.standard_normal((rows, d)).astype(np.float32)
+    w1 = (rng.standard_normal((E_loc, inter, d)) / np.sqrt(d)).astype(np.float32)
+    w3 = (rng.standard_normal((E_loc, inter, d)) / np.sqrt(d)).astype(np.float32)
+    w2 = (rng.standard_normal((E_loc, d, inter)) / (12 * np.sqrt(inter))).astype(np.float32)
+    if dtype == "bf16":
+        q = lambda a: gen.f32_to_bf16_bits(a)
+        x32, w1, w3, w2 = (gen.bf16_bits_to_f32(q(a)) for a in (x32, w1, w3, w2))
+        tdt, cdt = torch.bfloat16, capi.CAP_DTYPE_BF16
+        dev = lambda a: torch.from_numpy(q(a).view(np.int16)).view(torch.bfloat16).cuda()
+    else:
+        tdt, cdt = torch.float32, capi.CAP_DTYPE_F32
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+    max_rows = rows + 5
+    xs = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
+    xs[:rows] = dev(x32)
+    y = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                     dtype=torch.uint8, device="cuda")
+    capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, xs, torch.from_numpy(offs).cuda(), dev(w1), dev(w3),
+                        dev(w2), y, ws)
+    torch.cuda.synchronize()
+    got = y[:rows].float().cpu().numpy()
+    ref = oracle.expert_ffn(x32, offs, [(w1[l], w3[l], w2[l]) for l in range(E_loc)])
+    return got, ref
+
+
+@pytest.mark.parametrize("counts", [[300, 1, 0, 513], [256, 256], [1], [0, 0, 700, 40, 1000, 3]])
+def test_ffn_bf16_ragged_experts(counts):
+    got, ref = _ffn_direct("bf16", len(counts), 512, 384, counts, seed=len(counts))
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+
+
+def test_ffn_f32_ragged_experts():
+    got, ref = _ffn_direct("f32", 3, 128, 256, [70, 0, 131], seed=3)
+    ok, worst = C.within_tol(got, ref, atol=1e-5, rtol=1e-4)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-5
+
+
+@pytest.mark.parametrize("name,kind,p", [("c2", "coact", 0.3), ("c2", "seq", 0.0), ("c4", "coact", 0.1)])
+def test_ffn_full_size_sampled_rows(name, kind, p):
+    """Rank 0's expert FFN at the workload's real shape; sampled rows vs the oracle."""
+    case = C.Case(name, gen.CONFIGS[name], kind, p)
+    cfg = case.cfg
+    er, el = C.placement(name, kind, p, 5.0)
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = _layer(case, x=x)
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    L.front()
+    L.gather(0)
+    L.ffn(0)
+    torch.cuda.synchronize()
+    rows = L.rank_rows(0)
+    rng = np.random.default_rng(1)
+    sample = np.sort(rng.choice(rows, size=min(48, rows), replace=False))
+    eo = lay["expert_offsets"]
+    xs_all = gen.bf16_bits_to_f32(oracle.expert_gather(x, r["idx"], r["keep"], lay["slot_pos"], eo, er, cfg.R, 0))
+    got = L.Y[torch.from_numpy(sample).cuda()].float().cpu().numpy()
+    ids = C.local_experts(er, el, 0, cfg.E_loc)
+    ref = np.empty_like(got, dtype=np.float64)
+    for l in range(cfg.E_loc):
+        a, b = eo[l] - eo[0], eo[l + 1] - eo[0]
+        sel = np.where((sample >= a) & (sample < b))[0]
+        if len(sel):
+            W1, W3, W2 = gen.expert_weights_f32(cfg, ids[l])
+            ref[sel] = oracle.swiglu_rows(xs_all[sample[sel]], W1, W3, W2)
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+
+
+# ---------------------------------------------------------------- combine / whole layer
+@pytest.mark.parametrize("cfgname,kind,p", [("c1", "seq", 0.3), ("c1u", "seq", 0.3), ("c1u", "coact", 0.0)])
+def test_layer_tiny_fp32_end_to_end(cfgname, kind, p):
+    """All 4 ranks on the GPU: gather -> FFN -> dest reduce; then every source
+    rank's src reduce, against the oracle's independent dense Eq. 1 path."""
+    cfg = gen.CONFIGS[cfgname]
+    case = C.Case(cfgname, cfg, kind, p)
+    er, el = C.placement(cfgname, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = DeviceLayer(cfg, gen.logits(cfg), x, er, el, p, 5.0)
+    for rank in range(cfg.R):
+        L.set_rank_weights(rank, *C.rank_weights(cfg, er, el, rank))
+    L.front()
+    for rank in range(cfg.R):
+        L.gather(rank)
+        L.ffn(rank)
+        L.dest_reduce(rank)
+    r = oracle.route_prune(gen.logits(cfg), cfg.k, er, cfg.ranks_per_node, cfg.tokens_per_rank, 5.0, p)
+    wts = {e: gen.expert_weights_f32(cfg, e) for e in range(cfg.E)}
+    for s in range(cfg.R):
+        L.src_reduce(s)
+        torch.cuda.synchronize()
+        toks = np.arange(s * cfg.tokens_per_rank, (s + 1) * cfg.tokens_per_rank)
+        ref = oracle.dense_moe_rows(toks, x[toks], r, lambda e: wts[e])
+        got = L.host("y")
+        ok, worst = C.within_tol(got, ref, atol=1e-6 if cfgname == "c1" else 1e-5, rtol=1e-4)
+        assert ok, (s, worst)
+        assert C.rel_fro(got, ref) <= 1e-5
+
+
+def test_combine_bf16_full_size_sampled():
+    """C2 coact p=0.3, rank 0: destination reduce of the real FFN output on
+    sampled received tokens, and source reduce of seeded returned rows."""
+    name, kind, p = "c2", "coact", 0.3
+    cfg = gen.CONFIGS[name]
+    case = C.Case(name, cfg, kind, p)
+    er, el = C.placement(name, kind, p, 5.0)
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = _layer(case, x=x)
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    L.front()
+    L.gather(0)
+    L.ffn(0)
+    L.dest_reduce(0)
+    torch.cuda.synchronize()
+    U0 = int(lay["recv_offsets"][1])
+    rng = np.random.default_rng(2)
+    sample = np.sort(rng.choice(U0, size=32, replace=False))
+    got = L.parts[torch.from_numpy(sample).cuda()].float().cpu().numpy()
+    ref = np.zeros(got.shape, np.float64)
+    for i, u in enumerate(sample):
+        t = int(lay["recv_token"][u])
+        for s in range(cfg.k):
+            if r["keep"][t, s] and er[r["idx"][t, s]] == 0:
+                W1, W3, W2 = gen.expert_weights_f32(cfg, int(r["idx"][t, s]))
+                xt = gen.bf16_bits_to_f32(x[t:t + 1])
+                ref[i] += float(r["wp"][t, s]) * oracle.swiglu_rows(xt, W1, W3, W2)[0]
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+    # source reduce over seeded returned rows for every device
+    n_recv = int(lay["recv_offsets"][-1])
+    parts = gen.random_rows(n_recv, cfg.d, "bf16", salt=3)
+    L.parts[:n_recv] = torch.from_numpy(parts.view(np.int16)).view(torch.bfloat16).cuda()
+    L.src_reduce(0)
+    torch.cuda.synchronize()
+    ref = oracle.src_reduce(gen.bf16_bits_to_f32(parts), r, lay, er, cfg.R, cfg.tokens_per_rank, 0, cfg.d)
+    got = L.y.float().cpu().numpy()
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
