@@ -1,0 +1,329 @@
+#!/usr/bin/env python3
+"""Benchmark of the CAP expert-parallel MoE layer hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input, inputs
+resident in HBM:
+  route + prune (all T tokens of all virtual ranks), dispatch layout,
+  co-activation counts, expert gather for rank 0, rank 0's grouped SwiGLU FFN,
+  destination reduce for rank 0, [shared experts], source reduce for rank 0.
+`value` = rank 0's tokens carried through the layer per second
+(tokens_per_rank / step time; the step also routes every other virtual rank's
+tokens, which a real rank would not do).
+
+The rows every other rank returns to rank 0 are stand-in values in HBM (on a
+real system they arrive by all-to-all); rank 0's own rows are recomputed every
+step.  The dominant kernel is the grouped FFN (two GEMM launches per call),
+timed live with HIP events on the stream it runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routed tokens/s per MoE layer (1 GPU) + %HBM/%MFMA peak; send bytes/token"
+PEAK_BF16_TFLOPS = 2500.0          # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0              # MI355X HBM3E
+PROFILES = os.path.join(ROOT, "profiles")
+FFN_SOURCE = os.path.join(ROOT, "paper_2607_05116_amd", "csrc", "expert_ffn.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", default="c2", help="workload: c1..c5 (default c2, Qwen3-shaped)")
+    ap.add_argument("--placement", default="coact", choices=["coact", "seq"])
+    ap.add_argument("--p", type=float, default=0.3, help="pruning threshold (paper: 0.3 for Qwen3)")
+    ap.add_argument("--c", type=float, default=5.0, help="inter-node cost")
+    ap.add_argument("--rank", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--cpu-stride", type=int, default=4, help="oracle FFN runs every n-th rank-0 row")
+    return ap.parse_args()
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def rank_weights(gen, cfg, er, el, rank):
+    import numpy as np
+    ids = [-1] * cfg.E_loc
+    for e in range(cfg.E):
+        if er[e] == rank:
+            ids[el[e]] = e
+    ws = [gen.expert_weights(cfg, e) for e in ids]
+    return tuple(np.stack([w[i] for w in ws]) for i in range(3))
+
+
+def product_placement(cfg, p, c):
+    """CAP offline steps 1-2 on the GPU path: pruned routing trace under
+    sequential placement -> co-activation counts -> Algorithm 1 + node stage."""
+    import dataclasses
+    import numpy as np
+    from paper_2607_05116_amd import placement
+    from paper_2607_05116_amd.layer import DeviceLayer
+    from workloads import generator as gen
+    er0, el0 = gen.sequential_placement(cfg)
+    tcfg = dataclasses.replace(cfg, T=cfg.trace_tokens, d=8)
+    trace = gen.trace_logits(cfg)
+    Lt = DeviceLayer(tcfg, trace, np.zeros((tcfg.T, 8), np.uint16), er0, el0, p, c, row_cap=8, recv_cap=8)
+    Lt.route()
+    Lt.coactivation()
+    C = Lt.host("coact").view(np.uint32)
+    return placement.coactivation_placement(C, cfg.R, cfg.ranks_per_node, gen.random_order(cfg.E, 0, 0),
+                                            gen.random_order(cfg.R, 0, 1))
+
+
+def file_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profile(workload_key: str):
+    """HBM bytes per FFN call from a committed rocprofv3 counter summary, if it
+    was taken on the current FFN source (else None)."""
+    path = os.path.join(PROFILES, f"expert_ffn_{workload_key}_hbm_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha256_16") != file_hash(FFN_SOURCE):
+        return None
+    return rec.get("bytes_per_call")
+
+
+def cpu_baseline(cfg, p, c, logits, x, stride):
+    """The oracle as it stands, timed on this host on a bounded sample."""
+    import numpy as np
+    import oracle
+    from oracle import placement as oplace
+    from workloads import generator as gen
+    threads = min(16, os.cpu_count() or 1)
+    er0, _ = gen.sequential_placement(cfg)
+    tr = oracle.route_prune(gen.trace_logits(cfg), cfg.k, er0, cfg.ranks_per_node,
+                            cfg.trace_tokens // cfg.R, c, p)
+    C = oracle.coactivation(tr["idx"], tr["keep"], cfg.E)
+    er, el = oplace.coactivation_placement(C, cfg.R, cfg.ranks_per_node, gen.random_order(cfg.E, 0, 0).tolist(),
+                                           gen.random_order(cfg.R, 0, 1).tolist())
+    er, el = np.array(er, np.int32), np.array(el, np.int32)
+    t0 = time.perf_counter()
+    r = oracle.route_prune(logits, cfg.k, er, cfg.ranks_per_node, cfg.tokens_per_rank, c, p)
+    lay = oracle.dispatch_layout(r["idx"], r["keep"], r["mask"], er, el, cfg.R, cfg.ranks_per_node,
+                                 cfg.tokens_per_rank, cfg.E)
+    oracle.coactivation(r["idx"], r["keep"], cfg.E)
+    t_front = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    xs = oracle.expert_gather(x, r["idx"], r["keep"], lay["slot_pos"], lay["expert_offsets"], er, cfg.R, 0)
+    t_gather = time.perf_counter() - t0
+    xs32 = gen.bf16_bits_to_f32(xs) if cfg.dtype == "bf16" else xs
+    eo = lay["expert_offsets"]
+    rows0 = int(eo[cfg.E_loc] - eo[0])
+    ids = [-1] * cfg.E_loc
+    for e in range(cfg.E):
+        if er[e] == 0:
+            ids[el[e]] = e
+    t_ffn, n_sample = 0.0, 0
+    for l in range(cfg.E_loc):
+        a, b = int(eo[l] - eo[0]), int(eo[l + 1] - eo[0])
+        rows = np.arange(a, b)[::stride]
+        if len(rows) == 0:
+            continue
+        W = gen.expert_weights_f32(cfg, ids[l])
+        t0 = time.perf_counter()
+        oracle.swiglu_rows(xs32[rows], *W, nthreads=threads)
+        t_ffn += time.perf_counter() - t0
+        n_sample += len(rows)
+    t_ffn_full = t_ffn * rows0 / max(1, n_sample)
+    Y = np.zeros((rows0, cfg.d), np.float32)
+    t0 = time.perf_counter()
+    oracle.dest_reduce(Y, r, lay, er, cfg.R, 0, cfg.d)
+    t_dest = time.perf_counter() - t0
+    parts = np.zeros((int(lay["recv_offsets"][-1]), cfg.d), np.float32)
+    t0 = time.perf_counter()
+    oracle.src_reduce(parts, r, lay, er, cfg.R, cfg.tokens_per_rank, 0, cfg.d)
+    t_src = time.perf_counter() - t0
+    total = t_front + t_gather + t_ffn_full + t_dest + t_src
+    return {
+        "value": cfg.tokens_per_rank / total,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"full routing/layout/co-activation of all {cfg.T} tokens ({t_front:.2f} s, 1 thread), "
+                   f"rank-0 gather ({t_gather:.2f} s), fp64 SwiGLU on every {stride}th of {rows0} rank-0 rows "
+                   f"({n_sample} rows, {t_ffn:.2f} s on {threads} threads, scaled x{rows0 / max(1, n_sample):.2f}), "
+                   f"destination + source reduce of rank 0 ({t_dest + t_src:.2f} s, 1 thread); "
+                   f"host: {cpu_model()}"),
+    }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures the hot path on one GPU (virtual expert-parallel ranks); "
+              f"--gpus {args.gpus} / WORLD_SIZE={world} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2607_05116_amd.layer import DeviceLayer
+    from workloads import generator as gen
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = gen.CONFIGS[args.config]
+    rank = args.rank
+    t_setup = time.perf_counter()
+    logits = gen.logits(cfg)
+    x = gen.activations(cfg)
+    if args.placement == "coact":
+        er, el = product_placement(cfg, args.p, args.c)
+    else:
+        er, el = gen.sequential_placement(cfg)
+    L = DeviceLayer(cfg, logits, x, er, el, args.p, args.c)
+    L.set_rank_weights(rank, *rank_weights(gen, cfg, er, el, rank))
+    if cfg.n_shared:
+        L.set_shared_weights(*gen.shared_weights(cfg))
+    L.front()
+    torch.cuda.synchronize()
+    n_recv = int(L.host("recv_offsets")[-1])
+    g = torch.Generator(device="cuda").manual_seed(1234)
+    L.parts[:n_recv] = (torch.randn((n_recv, cfg.d), generator=g, device="cuda") * 0.05).to(L.tdt)
+    log(f"setup {time.perf_counter() - t_setup:.1f} s; rank-{rank} rows {L.rank_rows(rank)}, received rows {n_recv}")
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        L.step(rank)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ffn_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(K):
+        L.front()
+        L.gather(rank)
+        ffn_ev[i][0].record(stream)
+        L.ffn(rank)
+        ffn_ev[i][1].record(stream)
+        L.dest_reduce(rank)
+        L.shared_ffn(rank)
+        L.src_reduce(rank)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_per_step = t_start.elapsed_time(t_end) / K
+    ffn_ms = sum(a.elapsed_time(b) for a, b in ffn_ev) / K
+    log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
+
+    # per-stage breakdown (separate, untimed pass)
+    stages = ["route", "layout", "coact", "gather", "ffn", "dest", "shared", "src"]
+    fns = [L.route, L.layout, L.coactivation, lambda: L.gather(rank), lambda: L.ffn(rank),
+           lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank)]
+    reps = 5
+    acc = {s: 0.0 for s in stages}
+    for _ in range(reps):
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
+        evs[0].record(stream)
+        for j, fn in enumerate(fns):
+            fn()
+            evs[j + 1].record(stream)
+        torch.cuda.synchronize()
+        for j, s in enumerate(stages):
+            acc[s] += evs[j].elapsed_time(evs[j + 1]) / reps
+    stage_ms = {s: round(v, 5) for s, v in acc.items()}
+
+    rows = L.rank_rows(rank)
+    flops = 6.0 * cfg.d * cfg.inter * rows
+    achieved = flops / (ffn_ms * 1e-3) / 1e12
+    workload_key = f"{cfg.name}_{args.placement}_p{args.p:g}"
+    traffic = traffic_from_profile(workload_key)
+    totals = L.host("totals").astype(np.int64)
+    eb = cfg.elem_bytes
+    send_copies = int(totals[1] + totals[2])
+    loads = np.diff(L.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
+    # HBM roofline context for the row movers (algorithmic bytes / measured time)
+    U = int(L.host("recv_offsets")[rank + 1] - L.host("recv_offsets")[rank])
+    mask = L.host("mask").view(np.uint64)[rank * cfg.tokens_per_rank:(rank + 1) * cfg.tokens_per_rank]
+    n_dev_src = int(sum(bin(int(m)).count("1") for m in mask))
+    kbytes = {
+        "route": cfg.T * cfg.E * 4 + cfg.T * cfg.k * 9 + cfg.T * 8,
+        "gather": (U + rows) * cfg.d * eb + rows * 4,
+        "dest": rows * (cfg.d * eb + 8) + U * cfg.d * eb,
+        "src": (n_dev_src + cfg.tokens_per_rank * (2 if cfg.n_shared else 1)) * cfg.d * eb,
+    }
+    hbm = {s: round(kbytes[s] / (stage_ms[s] * 1e-3) / 1e9, 1) for s in kbytes if stage_ms[s] > 0}
+
+    result = {
+        "metric": METRIC,
+        "value": cfg.tokens_per_rank / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded latent-topic router logits, N(0,1) activations, scaled random-init weights)",
+        "config": {
+            "workload": (f"{cfg.name}: MoE layer T={cfg.T} tokens ({cfg.R} virtual ranks x {cfg.tokens_per_rank}), "
+                         f"d={cfg.d}, E={cfg.E} top-{cfg.k}, SwiGLU inter={cfg.inter}"
+                         + (f" + {cfg.n_shared} shared x {cfg.shared_inter}" if cfg.n_shared else "")
+                         + f", {args.placement} placement, p={args.p:g}, c={args.c:g}, FFN/combine on rank {rank}"),
+            "T": cfg.T, "tokens_per_rank": cfg.tokens_per_rank, "d": cfg.d, "E": cfg.E, "k": cfg.k,
+            "inter": cfg.inter, "R": cfg.R, "ranks_per_node": cfg.ranks_per_node,
+            "placement": args.placement, "p": args.p, "c": args.c, "rank": rank,
+            "parallelism": "1 GPU, virtual EP ranks",
+        },
+        "roofline": {
+            "kernel": "cap_expert_ffn (gate/up GEMM + down GEMM launches), rank 0",
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+            "flops_per_call": flops, "rows": rows, "avg_call_ms": ffn_ms,
+        },
+        "aux": {
+            "stage_ms": stage_ms,
+            "stage_hbm_GBs": hbm,
+            "send_bytes_per_token": send_copies * cfg.d * eb / cfg.T,
+            "send_bytes_per_token_intra": int(totals[1]) * cfg.d * eb / cfg.T,
+            "send_bytes_per_token_inter": int(totals[2]) * cfg.d * eb / cfg.T,
+            "device_per_token": int(totals[0]) / cfg.T,
+            "node_per_token": int(totals[3]) / cfg.T,
+            "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
+            "rank_rows": rows, "rank_received_tokens": U,
+            "host_wall_ms_per_step": 1e3 * wall / K,
+        },
+    }
+    if not args.no_cpu:
+        log("timing the CPU oracle on a bounded sample ...")
+        result["cpu_baseline"] = cpu_baseline(cfg, args.p, args.c, logits, x, args.cpu_stride)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,116 @@
+"""Host-side checks that need no GPU: the C ABI library loads and exports
+every symbol include/cap.h declares, argument validation rejects bad calls
+before launching anything, and bench.py refuses more than one GPU."""
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cap.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(cap_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def capi():
+    from paper_2607_05116_amd import capi as c
+    return c
+
+
+def test_library_exports_every_declared_symbol(capi):
+    names = _declared()
+    assert "cap_route_prune" in names and len(names) >= 9
+    lib = ctypes.CDLL(capi.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(capi.EXPORTS) == names
+
+
+def test_status_strings_and_version(capi):
+    assert capi.status_string(0) == "CAP_OK"
+    assert "workspace" in capi.status_string(-3)
+    assert capi.cap_version() >= 100
+
+
+def _topo(capi, **over):
+    kw = dict(E=16, R=4, ranks_per_node=4, T=256, k=2)
+    kw.update(over)
+    t = capi.make_topology(kw["E"], kw["R"], kw["ranks_per_node"], kw["T"], kw["k"], 0x1000, 0x2000, 5.0)
+    return t
+
+
+@pytest.mark.parametrize("over", [dict(k=0), dict(k=9), dict(E=300), dict(E=18), dict(R=65, E=130, T=260),
+                                  dict(T=255), dict(ranks_per_node=3)])
+def test_route_prune_rejects_bad_topology(capi, over):
+    t = _topo(capi, **over)
+    st = capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None)
+    assert st == capi.CAP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("p", [-0.1, 1.0, 1.5, float("nan")])
+def test_route_prune_rejects_bad_threshold(capi, p):
+    t = _topo(capi)
+    st = capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, p, 0x4000, 0x5000, 0x6000, 0x7000, None)
+    assert st == capi.CAP_ERR_INVALID_ARG
+
+
+def test_route_prune_rejects_null_and_bad_cost(capi):
+    t = _topo(capi)
+    assert capi._lib.cap_route_prune(ctypes.byref(t), None, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
+    t.inter_node_cost = 0.5
+    assert capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
+
+
+def test_workspace_checks(capi):
+    t = _topo(capi)
+    need = capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, t)
+    assert need > 0
+    lay = capi.Layout(*([0x10000] * 10))
+    st = capi._lib.cap_dispatch_layout(ctypes.byref(t), 0x3000, 0x4000, 0x5000, ctypes.byref(lay), 0x8000,
+                                       need - 1, None)
+    assert st == capi.CAP_ERR_WORKSPACE
+    n = capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, 2048, 768, 1000, capi.CAP_DTYPE_BF16)
+    assert n == 1000 * 768 * 2
+    st = capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2048, 768, 1000, 0x1000, 0x2000, 0x3000, 0x4000,
+                                  0x5000, 0x6000, 0x7000, n - 1, None)
+    assert st == capi.CAP_ERR_WORKSPACE
+
+
+def test_ffn_rejects_unsupported_shapes(capi):
+    args = (0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, 0x7000, 1 << 30, None)
+    assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2000, 768, 100, *args) == capi.CAP_ERR_UNSUPPORTED
+    assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2048, 700, 100, *args) == capi.CAP_ERR_UNSUPPORTED
+    assert capi._lib.cap_expert_ffn(7, 4, 2048, 768, 100, *args) == capi.CAP_ERR_UNSUPPORTED
+    assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 0, 2048, 768, 100, *args) == capi.CAP_ERR_INVALID_ARG
+
+
+def test_permute_and_combine_validation(capi):
+    t = _topo(capi)
+    lay = capi.Layout(*([0x10000] * 10))
+    bad_rank = capi._lib.cap_permute(ctypes.byref(t), 0, 4, 1, 128, 0x1000, 0x2000, 0x3000, 0x4000,
+                                     ctypes.byref(lay), 0x5000, 10, None)
+    assert bad_rank == capi.CAP_ERR_INVALID_ARG
+    bad_mode = capi._lib.cap_permute(ctypes.byref(t), 5, 0, 1, 128, 0x1000, 0x2000, 0x3000, 0x4000,
+                                     ctypes.byref(lay), 0x5000, 10, None)
+    assert bad_mode == capi.CAP_ERR_UNSUPPORTED
+    bad_d = capi._lib.cap_permute(ctypes.byref(t), 0, 0, 1, 12, 0x1000, 0x2000, 0x3000, 0x4000,
+                                  ctypes.byref(lay), 0x5000, 10, None)
+    assert bad_d == capi.CAP_ERR_INVALID_ARG
+    small_out = capi._lib.cap_combine(ctypes.byref(t), 1, 0, 1, 128, 0x1000, 10, 0x2000, 0x3000, 0x4000,
+                                      0x5000, ctypes.byref(lay), None, 0x6000, 63, None)
+    assert small_out == capi.CAP_ERR_INVALID_ARG
+
+
+def test_bench_refuses_more_than_one_gpu():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
