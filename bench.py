@@ -46,7 +46,22 @@ def parse():
     ap.add_argument("--rank", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-stride", type=int, default=4, help="oracle FFN runs every n-th rank-0 row")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only run 3 device-to-device copies of MIB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy(mib: int):
+    """A plain copy of known size: reads and writes mib MiB per launch, so HBM
+    byte counters of other kernels can be scaled against it."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 3}), flush=True)
 
 
 def log(msg):
@@ -183,6 +198,10 @@ def main():
         print(f"bench.py measures the hot path on one GPU (virtual expert-parallel ranks); "
               f"--gpus {args.gpus} / WORLD_SIZE={world} is not supported", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
 
     import numpy as np
     import torch

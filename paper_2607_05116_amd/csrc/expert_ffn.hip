@@ -7,13 +7,13 @@
 //   down      Y[m][o] = (H W2^T)[m][o]                         (K = inter)
 //
 // bf16 path (gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation):
-//   * Block tile BM x BN x 64, waves arranged WAVES_M x WAVES_N, each wave a
+//   * Block tile BM x BN (K sliced by 32), waves arranged WAVES_M x WAVES_N, each wave a
 //     (BM/WAVES_M) x (BN/WAVES_N) sub-tile of 32x32 MFMA blocks.
 //   * Operands are both K-contiguous (token rows of X / H; weight rows of W).
-//     Global -> registers -> LDS, double-buffered, one barrier per K step.
-//     LDS rows are 128 B (64 bf16); the 16-byte chunk c of row r is stored at
-//     chunk c ^ (r & 7) so the MFMA fragment reads (8 consecutive rows, same
-//     chunk) hit distinct banks.
+//     gfx950 direct-to-LDS loads (global_load_lds_dwordx4) fill a 4-stage LDS
+//     ring of 32-wide K slices, three stages ahead of the MFMAs, with no
+//     staging registers; one barrier per K slice.  The next tile's first
+//     stages are issued before the current tile's epilogue stores.
 //   * The MFMA is issued with the weight fragment as its first operand, so a
 //     lane's 16 accumulators hold 4 consecutive output columns per register
 //     group and the epilogue stores 8 bytes at a time.
@@ -30,7 +30,6 @@
 namespace cap {
 namespace {
 
-constexpr int kBK = 64;           // K per LDS stage (bf16): one 128-byte row
 constexpr int kMaxExpertsLocal = kMaxE;
 
 // ------------------------------------------------------------------ tile scheduler
@@ -78,23 +77,86 @@ __device__ __forceinline__ int worker_id() {
     return (G % 8 == 0) ? (b % 8) * (G / 8) + b / 8 : b;
 }
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// silu(g) = g * sigmoid(g); hardware exp2 and reciprocal (about 1 ulp each),
+// far inside the bf16 rounding that H then takes.
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
+// LDS ring of kStages stages; a stage holds the A tile [BM][32] and the B tile
+// [BN][32] (bf16, 64-byte rows).  16-byte chunk c of row r sits at physical
+// chunk c ^ lds_swz(r): fragment reads (rows r..r+15, one chunk) then hit
+// distinct banks for both 128- and 256-byte bank windows.
+constexpr int kStageK = 32;                 // K per stage
+constexpr int kStages = 4;                  // prefetch distance kStages - 1
+constexpr int kRowB = kStageK * 2;          // bytes per LDS row
+
+__device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+
+// Workgroup barrier without the memory fence that __syncthreads() carries (the
+// fence would drain every in-flight prefetch).  LDS visibility is ensured by
+// explicit vmcnt waits on the direct-to-LDS loads and the compiler's lgkmcnt
+// waits on ds_read; the empty asm statements keep memory accesses from being
+// moved across the barrier.
+__device__ __forceinline__ void block_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// Wait until at most n of this wave's vector-memory operations are in flight.
+// Loads complete in issue order, so with n = (loads issued after the stage we
+// need) that stage has landed in LDS; pending stores only make it stricter.
+__device__ __forceinline__ void wait_vmem(int n) {
+    if (n >= 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    else if (n >= 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// One wave-wide copy global -> LDS (gfx950 global_load_lds_dwordx4): lane i
+// reads 16 bytes at base + voff_i and they land at LDS byte lds_addr + 16 * i.
+// `base` is wave-uniform (scalar registers), voff a 32-bit per-lane byte
+// offset.  Issued as inline assembly so the compiler's wait-count pass does not
+// treat every later LDS read as aliasing it (it would drain all in-flight
+// stages); the kernel waits on these loads explicitly with wait_vmem().  The
+// instruction's immediate offset stays 0 (it would shift the LDS address too).
+// Because the compiler does not see the instruction, it also does not insert
+// the wait states the hardware needs before it: a VALU write of an SGPR
+// (v_readfirstlane of the base) needs 5 wait states before a vector-memory
+// instruction reads that SGPR, and an SALU write of M0 needs 1 before an LDS
+// DMA.  The s_nop 4 inside the statement provides 5.
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
+    // The base is uniform by construction; say so, so it lives in scalar
+    // registers.  readfirstlane returns a signed int: widen through uint32_t so
+    // the low word is zero-extended, never sign-extended.
+    const uint64_t b = reinterpret_cast<uint64_t>(base);
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+    const void* sbase = reinterpret_cast<const void*>((hi << 32) | lo);
+    asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase),
+                 "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool GATEUP>
 __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
     uint16_t* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K,
     int N_out) {
-    constexpr int NT = WAVES_M * WAVES_N * kWave;
+    constexpr int NW = WAVES_M * WAVES_N;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int MI = WM / 32, NJ = WN / 32;
-    constexpr int A_LD = BM * 8 / NT;      // 16-byte chunks per thread per stage
-    constexpr int B_LD = BN * 8 / NT;
-    static_assert(BM * 8 % NT == 0 && BN * 8 % NT == 0, "tile / thread mismatch");
+    constexpr int ROWS_PER_LOAD = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
+    constexpr int A_LD = BM / ROWS_PER_LOAD / NW;          // direct loads per wave per stage
+    constexpr int B_LD = BN / ROWS_PER_LOAD / NW;
+    constexpr int STAGE_B = (BM + BN) * kRowB;
+    constexpr int LOADS_PER_STAGE = A_LD + B_LD;
+    static_assert(BM % (ROWS_PER_LOAD * NW) == 0 && BN % (ROWS_PER_LOAD * NW) == 0, "load split");
+    static_assert(LOADS_PER_STAGE == 8, "wait_vmem assumes 8 loads per stage");
     static_assert(!GATEUP || (WN % 64 == 0), "gate/up pairs need 64-column wave tiles");
+    static_assert(ROWS_PER_LOAD * NW >= 32 || !GATEUP, "a direct load must stay inside one W1/W3 block");
 
-    __shared__ __attribute__((aligned(16))) uint8_t lds[2][(BM + BN) * 128];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE_B];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
     __shared__ int row_begin[kMaxExpertsLocal];
     __shared__ int row_end[kMaxExpertsLocal];
@@ -102,50 +164,78 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     build_schedule<BM>(row_offsets, E_loc, max_rows, mt_prefix, row_begin, row_end);
     const int n_tiles = GATEUP ? N_out / (BN / 2) : N_out / BN;
     const int total = mt_prefix[E_loc] * n_tiles;
-    const int KT = K / kBK;
+    const int KT = K / kStageK;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
     const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
 
-    for (int tile = worker_id(); tile < total; tile += gridDim.x) {
+    // direct-load lane mapping: lane l writes LDS row (l >> 2), physical chunk
+    // (l & 3) of its 1 KiB block, so it fetches logical chunk (l & 3) ^ swz.
+    const int ld_row = lane >> 2;
+    const int ld_col = (((lane & 3) ^ lds_swz(ld_row)) * 8);        // elements
+    // fragment lane mapping (row r = ... + (lane & 31); swz depends on lane & 31 only)
+    const int fr_row = lane & 31;
+    const int fr_swz = lds_swz(fr_row);
+    const int fr_half = lane >> 5;
+
+    // Per-tile load sources: wave-uniform byte bases (scalar) plus per-lane
+    // 32-bit byte offsets.  A rows past the expert's end are clamped to its
+    // last row (their results are never stored).
+    struct TileSrc {
+        const char* a;              // A + row0 * K
+        uint32_t a_off[A_LD];       // lane offsets within the tile rows
+        const char* b[B_LD];        // row block of each B load
+    };
+    const uint32_t b_lane_off = static_cast<uint32_t>(ld_row * K + ld_col) * 2u;
+    auto tile_sources = [&](int tile, int& l, int& row0, int& rows_valid, int& nt) {
+        TileSrc src;
         const int m_tile = tile / n_tiles;
-        const int nt = tile % n_tiles;
-        const int l = find_expert(mt_prefix, E_loc, m_tile);
-        const int row0 = row_begin[l] + (m_tile - mt_prefix[l]) * BM;
-        const int rows_valid = min(BM, row_end[l] - row0);
-
-        // This thread's 16-byte chunks: column kc, rows rbase + (NT/8)*i.  In LDS
-        // they sit at a_off0 + i*(NT/8)*128 (the XOR key r & 7 is the same for
-        // every i).  A rows are clamped into the expert; B rows are a fixed
-        // stride apart.
-        static_assert(NT / 8 >= 32 && (NT / 8) % 32 == 0, "chunk rows must keep the 32-row blocks");
-        const int kc = tid & 7, rbase = tid >> 3;
-        const int swz = (kc ^ (rbase & 7)) << 4;
-        const int a_off0 = rbase * 128 + swz;
-        const int b_off0 = BM * 128 + rbase * 128 + swz;
-        int a_row[A_LD];
+        nt = tile % n_tiles;
+        l = find_expert(mt_prefix, E_loc, m_tile);
+        row0 = row_begin[l] + (m_tile - mt_prefix[l]) * BM;
+        rows_valid = min(BM, row_end[l] - row0);
+        src.a = reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
 #pragma unroll
-        for (int i = 0; i < A_LD; ++i) a_row[i] = row0 + min(rbase + (NT / 8) * i, rows_valid - 1);
-        const uint16_t* Acol = A + kc * 8;
-        // B chunk i covers tile row rbase + (NT/8)*i.
-        //   gate/up: 32-row block q = ((NT/8)*i + rbase) / 32 alternates W1 / W3
-        //   down:    row n = nt*BN + rbase + (NT/8)*i of W2
-        const uint16_t* b0;
-        const uint16_t* b1;
-        if constexpr (GATEUP) {
-            const size_t off = (static_cast<size_t>(l) * N_out + nt * (BN / 2) + (rbase & 31)) * K + kc * 8;
-            b0 = B0 + off;
-            b1 = B1 + off;
-        } else {
-            b0 = B0 + (static_cast<size_t>(l) * N_out + nt * BN + rbase) * K + kc * 8;
-            b1 = b0;
+        for (int i = 0; i < A_LD; ++i) {
+            const int r = (wave * A_LD + i) * ROWS_PER_LOAD + ld_row;
+            src.a_off[i] = static_cast<uint32_t>(min(r, rows_valid - 1) * K + ld_col) * 2u;
         }
-        // B chunk i: source row offset (in elements) from b0 / b1.
-#define CAP_B_PTR(i)                                                                               \
-    (GATEUP ? ((((((NT / 8) * (i) + rbase) >> 5) & 1) ? b1 : b0) +                                  \
-               static_cast<size_t>((((NT / 8) * (i) + rbase) >> 5) >> 1) * 32 * K)                  \
-            : (b0 + static_cast<size_t>((NT / 8) * (i)) * K))
+#pragma unroll
+        for (int i = 0; i < B_LD; ++i) {
+            const int blk = wave_u * B_LD + i;                 // 16-row block of the B tile
+            size_t row;
+            const uint16_t* W = B0;
+            if constexpr (GATEUP) {
+                const int q = blk >> 1;                        // W1 / W3 alternate per 32 rows
+                W = (q & 1) ? B1 : B0;
+                row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + (q >> 1) * 32 + (blk & 1) * 16;
+            } else {
+                row = static_cast<size_t>(l) * N_out + nt * BN + blk * 16;
+            }
+            src.b[i] = reinterpret_cast<const char*>(W + row * K);
+        }
+        return src;
+    };
+    auto issue_stage = [&](const TileSrc& src, int kt) {
+        const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * STAGE_B);
+        const size_t kb = static_cast<size_t>(kt) * kStageK * 2;
+#pragma unroll
+        for (int i = 0; i < A_LD; ++i) lds_dma16(src.a + kb, src.a_off[i], st + (wave_u * A_LD + i) * 1024);
+#pragma unroll
+        for (int i = 0; i < B_LD; ++i)
+            lds_dma16(src.b[i] + kb, b_lane_off, st + BM * kRowB + (wave_u * B_LD + i) * 1024);
+    };
 
+    int tile = worker_id();
+    int l = 0, row0 = 0, rows_valid = 0, nt = 0;
+    TileSrc src;
+    if (tile < total) {
+        src = tile_sources(tile, l, row0, rows_valid, nt);
+        for (int s = 0; s < kStages - 1 && s < KT; ++s) issue_stage(src, s);
+    }
+    while (tile < total) {
         f32x16 acc[MI][NJ];
 #pragma unroll
         for (int i = 0; i < MI; ++i)
@@ -154,74 +244,59 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-        u32x4 ra[A_LD], rb[B_LD];
-#pragma unroll
-        for (int i = 0; i < A_LD; ++i)
-            ra[i] = *reinterpret_cast<const u32x4*>(Acol + static_cast<size_t>(a_row[i]) * K);
-#pragma unroll
-        for (int i = 0; i < B_LD; ++i) rb[i] = *reinterpret_cast<const u32x4*>(CAP_B_PTR(i));
-#pragma unroll
-        for (int i = 0; i < A_LD; ++i) *reinterpret_cast<u32x4*>(&lds[0][a_off0 + i * (NT / 8) * 128]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < B_LD; ++i) *reinterpret_cast<u32x4*>(&lds[0][b_off0 + i * (NT / 8) * 128]) = rb[i];
-        __syncthreads();
-
         for (int kt = 0; kt < KT; ++kt) {
-            const int cur = kt & 1;
-            if (kt + 1 < KT) {
-                const int koff = (kt + 1) * kBK;
+            wait_vmem(LOADS_PER_STAGE * min(kStages - 2, KT - 1 - kt));
+            block_barrier();                       // stage kt visible; stage kt-1 free
+            if (kt + kStages - 1 < KT) issue_stage(src, kt + kStages - 1);
+            const uint8_t* sa = lds + (kt % kStages) * STAGE_B;
+            const uint8_t* sb = sa + BM * kRowB;
+            bf16x8 fa[2][MI], fb[2][NJ];
 #pragma unroll
-                for (int i = 0; i < A_LD; ++i)
-                    ra[i] = *reinterpret_cast<const u32x4*>(Acol + static_cast<size_t>(a_row[i]) * K + koff);
+            for (int ks = 0; ks < 2; ++ks) {
+                const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
 #pragma unroll
-                for (int i = 0; i < B_LD; ++i) rb[i] = *reinterpret_cast<const u32x4*>(CAP_B_PTR(i) + koff);
+                for (int i = 0; i < MI; ++i)
+                    fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * WM + i * 32 + fr_row) * kRowB + pc);
+#pragma unroll
+                for (int j = 0; j < NJ; ++j)
+                    fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * WN + j * 32 + fr_row) * kRowB + pc);
             }
-            const uint8_t* sa = lds[cur];
-            const uint8_t* sb = lds[cur] + BM * 128;
 #pragma unroll
-            for (int ks = 0; ks < kBK / 16; ++ks) {
-                const int kc = 2 * ks + (lane >> 5);
-                bf16x8 fa[MI], fb[NJ];
-#pragma unroll
-                for (int i = 0; i < MI; ++i) {
-                    const int r = wm * WM + i * 32 + (lane & 31);
-                    fa[i] = *reinterpret_cast<const bf16x8*>(sa + r * 128 + ((kc ^ (r & 7)) << 4));
-                }
-#pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int r = wn * WN + j * 32 + (lane & 31);
-                    fb[j] = *reinterpret_cast<const bf16x8*>(sb + r * 128 + ((kc ^ (r & 7)) << 4));
-                }
+            for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
                 for (int i = 0; i < MI; ++i)
 #pragma unroll
                     for (int j = 0; j < NJ; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[j], fa[i], acc[i][j], 0, 0, 0);
-            }
-            if (kt + 1 < KT) {
-                uint8_t* dst = lds[cur ^ 1];
-#pragma unroll
-                for (int i = 0; i < A_LD; ++i) *reinterpret_cast<u32x4*>(&dst[a_off0 + i * (NT / 8) * 128]) = ra[i];
-#pragma unroll
-                for (int i = 0; i < B_LD; ++i) *reinterpret_cast<u32x4*>(&dst[b_off0 + i * (NT / 8) * 128]) = rb[i];
-            }
-            __syncthreads();
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+            // issue all fragment reads of the slice first, then the MFMAs
+            __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MI + NJ), 0);   // DS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, 2 * MI * NJ, 0);     // MFMA
+        }
+
+        // every wave is done with this tile's LDS: start the next tile's loads,
+        // then write this tile's outputs while they are in flight
+        block_barrier();
+        const int cur_l = l, cur_row0 = row0, cur_rows = rows_valid, cur_nt = nt;
+        (void)cur_l;
+        const int next = tile + gridDim.x;
+        if (next < total) {
+            src = tile_sources(next, l, row0, rows_valid, nt);
+            for (int s = 0; s < kStages - 1 && s < KT; ++s) issue_stage(src, s);
         }
 
         // epilogue: lane holds token row m = lane % 32 of each 32-row block and,
         // per register group g, output columns 8g + 4*(lane/32) + 0..3 of each
         // 32-column block.
-        const int m_lane = lane & 31;
-        const int n_sub = (lane >> 5) * 4;
+        const int n_sub = fr_half * 4;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
-            const int mr = wm * WM + i * 32 + m_lane;
-            if (mr >= rows_valid) continue;
-            uint16_t* crow = C + static_cast<size_t>(row0 + mr) * N_out;
+            const int mr = wm * WM + i * 32 + fr_row;
+            if (mr >= cur_rows) continue;
+            uint16_t* crow = C + static_cast<size_t>(cur_row0 + mr) * N_out;
             if constexpr (GATEUP) {
 #pragma unroll
                 for (int jp = 0; jp < NJ / 2; ++jp) {
-                    const int j0 = nt * (BN / 2) + (wn * WN / 64 + jp) * 32;
+                    const int j0 = cur_nt * (BN / 2) + (wn * WN / 64 + jp) * 32;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         float h[4];
@@ -237,7 +312,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
             } else {
 #pragma unroll
                 for (int j = 0; j < NJ; ++j) {
-                    const int c0 = nt * BN + wn * WN + j * 32;
+                    const int c0 = cur_nt * BN + wn * WN + j * 32;
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
                         uint2 v;
@@ -248,7 +323,9 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
                 }
             }
         }
+        tile = next;
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // ------------------------------------------------------------------ fp32 SIMT GEMM (small shapes)
