@@ -1,9 +1,14 @@
 // Token permutation and weighted combine (Sec. II-C; Eq. 1).
 //
-// Both are HBM-bound row movers.  One wave owns one row at a time; each lane
-// moves 16-byte pieces (8 bf16 or 4 fp32) so a wave touches 1 KiB per vector
-// access, fully coalesced.  The grids are persistent (grid-stride over rows)
-// and read the row counts from device memory, so nothing waits on the host.
+// All four kernels are HBM-bound row movers built the same way:
+//   * one wave owns one row piece at a time (a token's row, or a contiguous
+//     part of it when there are too few tokens to fill the chip);
+//   * the token's k routing slots are read one slot per lane, so a token's
+//     metadata costs one round of parallel loads; small per-launch tables
+//     (expert -> device, receive offsets, send bases) sit in LDS;
+//   * the wave compacts its valid slots into a uniform list with a ballot and
+//     then issues every 16-byte load of a batch before it uses any, so each
+//     lane keeps JB (x rows) loads in flight instead of one.
 //
 //   expert gather  (dest rank r)  read each received token once, write it to
 //                  every kept expert row of r (device-centric: one copy per
@@ -15,6 +20,11 @@
 //   src reduce     (rank s) per token of s: sum of the rows every kept device
 //                  returned (+ the shared experts' output).
 // Accumulation is fp32 in a fixed order (slot order / ascending device).
+//
+// A kept slot's row in rank r's expert-sorted buffer is slot_pos - (first row
+// of r); the slot is on r exactly when that difference falls inside r's row
+// range (pruned slots hold -1), so gather and dest reduce need no expert ->
+// device lookup.
 #include "cap_device.hpp"
 
 namespace cap {
@@ -22,224 +32,358 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWavesPerBlock = kThreads / kWave;
+constexpr int kTargetWaves = 8192;   // row pieces per launch worth splitting rows for
 
 struct Topo {
     int T, E, k, R, tpr, E_loc;
 };
 
-__device__ __forceinline__ int expert_rank_of(const int32_t* er, int e, const Topo& g) {
-    return static_cast<unsigned>(e) < static_cast<unsigned>(g.E) ? er[e] : -1;
+// Piece p of a row of vpr 16-byte chunks cut into `pieces` near-equal parts.
+struct Piece {
+    int begin, end;
+};
+__device__ __forceinline__ Piece row_piece(int vpr, int pieces, int p) {
+    const int per = (vpr + pieces - 1) / pieces;
+    const int b = min(vpr, p * per);
+    return Piece{b, min(vpr, b + per)};
 }
 
-// ---------------------------------------------------------------- expert gather
-template <typename V>
-__global__ __launch_bounds__(kThreads) void expert_gather_kernel(
-    Topo g, int rank, int vec_per_row, const V* __restrict__ x, const int32_t* __restrict__ idx,
-    const uint8_t* __restrict__ keep, const int32_t* __restrict__ er, const int32_t* __restrict__ slot_pos,
-    const int32_t* __restrict__ expert_offsets, const int32_t* __restrict__ recv_offsets,
-    const int32_t* __restrict__ recv_token, V* __restrict__ out, int out_rows) {
-    const int r0 = recv_offsets[rank];
-    const int U = min(recv_offsets[rank + 1] - r0, g.T * g.k - r0);
-    const int base = expert_offsets[rank * g.E_loc];
-    const int rows_r = min(expert_offsets[(rank + 1) * g.E_loc] - base, out_rows);
-    if (r0 < 0) return;
-    const int nwaves = gridDim.x * kWavesPerBlock;
-    for (int u = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < U; u += nwaves) {
-        const int t = recv_token[r0 + u];
-        if (static_cast<unsigned>(t) >= static_cast<unsigned>(g.T)) continue;
-        int dst[kMaxK];
+// Uniform list of the rows held by the lanes whose `row` is >= 0, in lane
+// (= slot) order; returns their count.  Lanes >= kMaxK never hold a row.
+__device__ __forceinline__ int compact_rows(int row, int (&rows)[kMaxK]) {
+    uint64_t vb = __ballot(row >= 0);
+    const int n = __popcll(vb);
 #pragma unroll
-        for (int s = 0; s < kMaxK; ++s) {
-            dst[s] = -1;
-            if (s < g.k) {
-                const size_t q = static_cast<size_t>(t) * g.k + s;
-                if (keep[q] && expert_rank_of(er, idx[q], g) == rank) {
-                    const int row = slot_pos[q] - base;
-                    dst[s] = (static_cast<unsigned>(row) < static_cast<unsigned>(rows_r)) ? row : -1;
-                }
-            }
-        }
-        const V* src = x + static_cast<size_t>(t) * vec_per_row;
-        for (int c = lane_id(); c < vec_per_row; c += kWave) {
-            const V v = src[c];
-#pragma unroll
-            for (int s = 0; s < kMaxK; ++s)
-                if (dst[s] >= 0) out[static_cast<size_t>(dst[s]) * vec_per_row + c] = v;
+    for (int j = 0; j < kMaxK; ++j) {
+        rows[j] = -1;
+        if (j < n) {
+            const int s = __ffsll(static_cast<unsigned long long>(vb)) - 1;
+            rows[j] = __builtin_amdgcn_readlane(row, s);
+            vb &= vb - 1;
         }
     }
+    return n;
 }
 
-// ---------------------------------------------------------------- send pack
-template <typename V>
-__global__ __launch_bounds__(kThreads) void send_pack_kernel(
-    Topo g, int src_rank, int vec_per_row, const V* __restrict__ x, const int32_t* __restrict__ idx,
-    const uint8_t* __restrict__ keep, const int32_t* __restrict__ er, const uint64_t* __restrict__ mask,
-    const int32_t* __restrict__ copy_row, const int32_t* __restrict__ send_counts,
-    const int32_t* __restrict__ send_offsets, V* __restrict__ out, int out_rows) {
-    __shared__ int32_t row0[kMaxR];   // send_offsets[s][d] - (rows of d from sources < s)
-    if (threadIdx.x < g.R) {
-        const int d = threadIdx.x;
-        int before = 0;
-        for (int s2 = 0; s2 < src_rank; ++s2) before += send_counts[s2 * g.R + d];
-        row0[d] = send_offsets[src_rank * g.R + d] - before;
-    }
-    __syncthreads();
-    int total = 0;
-    for (int d = 0; d < g.R; ++d) total += send_counts[src_rank * g.R + d];
-    total = min(total, out_rows);
-    const int nwaves = gridDim.x * kWavesPerBlock;
-    for (int i = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; i < g.tpr; i += nwaves) {
-        const int t = src_rank * g.tpr + i;
-        const uint64_t m = mask[t];
-        int dst[kMaxK];
-#pragma unroll
-        for (int s = 0; s < kMaxK; ++s) {
-            dst[s] = -1;
-            if (s < g.k) {
-                const size_t q = static_cast<size_t>(t) * g.k + s;
-                const int d = expert_rank_of(er, idx[q], g);
-                if (keep[q] && d >= 0 && d < g.R && ((m >> d) & 1ull)) {
-                    bool first = true;      // one row per device: the device's first kept slot writes it
-                    for (int s2 = 0; s2 < s; ++s2) {
-                        const size_t q2 = static_cast<size_t>(t) * g.k + s2;
-                        if (keep[q2] && expert_rank_of(er, idx[q2], g) == d) first = false;
-                    }
-                    const int row = row0[d] + copy_row[q];
-                    if (first && static_cast<unsigned>(row) < static_cast<unsigned>(total)) dst[s] = row;
-                }
-            }
-        }
-        const V* src = x + static_cast<size_t>(t) * vec_per_row;
-        for (int c = lane_id(); c < vec_per_row; c += kWave) {
-            const V v = src[c];
-#pragma unroll
-            for (int s = 0; s < kMaxK; ++s)
-                if (dst[s] >= 0) out[static_cast<size_t>(dst[s]) * vec_per_row + c] = v;
-        }
-    }
+__device__ __forceinline__ float lane_value(float v, int s) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), s));
 }
 
 // ---------------------------------------------------------------- row load / store helpers
-struct Bf16Row {
-    typedef uint4 V;                           // 8 bf16
+struct Bf16Row {                              // 8 bf16 per chunk
     static constexpr int kElems = 8;
-    __device__ static void load(const V& v, float* f) {
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    __device__ static void load(const u32x4& v, float* f) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            f[2 * i] = __uint_as_float(w[i] << 16);
-            f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+            f[2 * i] = __uint_as_float(v[i] << 16);
+            f[2 * i + 1] = __uint_as_float(v[i] & 0xFFFF0000u);
         }
     }
-    __device__ static V store(const float* f) {
-        V v;
-        v.x = pack_bf16x2(f[0], f[1]);
-        v.y = pack_bf16x2(f[2], f[3]);
-        v.z = pack_bf16x2(f[4], f[5]);
-        v.w = pack_bf16x2(f[6], f[7]);
+    __device__ static u32x4 store(const float* f) {
+        u32x4 v;
+        v[0] = pack_bf16x2(f[0], f[1]);
+        v[1] = pack_bf16x2(f[2], f[3]);
+        v[2] = pack_bf16x2(f[4], f[5]);
+        v[3] = pack_bf16x2(f[6], f[7]);
         return v;
     }
 };
 
-struct F32Row {
-    typedef float4 V;
+struct F32Row {                               // 4 fp32 per chunk
     static constexpr int kElems = 4;
-    __device__ static void load(const V& v, float* f) { f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w; }
-    __device__ static V store(const float* f) { return make_float4(f[0], f[1], f[2], f[3]); }
+    __device__ static void load(const u32x4& v, float* f) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) f[i] = __uint_as_float(v[i]);
+    }
+    __device__ static u32x4 store(const float* f) {
+        u32x4 v;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = __float_as_uint(f[i]);
+        return v;
+    }
 };
 
-// ---------------------------------------------------------------- dest reduce
-template <typename RowT>
-__global__ __launch_bounds__(kThreads) void dest_reduce_kernel(
-    Topo g, int rank, int vec_per_row, const typename RowT::V* __restrict__ Y,
-    const int32_t* __restrict__ idx, const float* __restrict__ w, const uint8_t* __restrict__ keep,
-    const int32_t* __restrict__ er, const int32_t* __restrict__ slot_pos,
+// Copy chunks [pc.begin, pc.end) of src to rows[0..n) of out.
+template <int JB>
+__device__ __forceinline__ void fan_out(const u32x4* __restrict__ src, u32x4* __restrict__ out, int vpr,
+                                        Piece pc, int n, const int (&rows)[kMaxK]) {
+    for (int c0 = pc.begin + lane_id(); c0 < pc.end; c0 += kWave * JB) {
+        u32x4 v[JB];
+#pragma unroll
+        for (int j = 0; j < JB; ++j) {
+            const int c = c0 + j * kWave;
+            if (c < pc.end) v[j] = src[c];
+        }
+#pragma unroll
+        for (int r = 0; r < kMaxK; ++r) {
+            if (r >= n) break;
+            u32x4* dst = out + static_cast<size_t>(rows[r]) * vpr;
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int c = c0 + j * kWave;
+                if (c < pc.end) dst[c] = v[j];
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------- expert gather
+template <int JB>
+__global__ __launch_bounds__(kThreads) void expert_gather_kernel(
+    Topo g, int rank, int vpr, int pieces, const u32x4* __restrict__ x, const int32_t* __restrict__ slot_pos,
     const int32_t* __restrict__ expert_offsets, const int32_t* __restrict__ recv_offsets,
-    const int32_t* __restrict__ recv_token, typename RowT::V* __restrict__ out, int in_rows, int out_rows) {
-    typedef typename RowT::V V;
+    const int32_t* __restrict__ recv_token, u32x4* __restrict__ out, int out_rows) {
     const int r0 = recv_offsets[rank];
+    if (r0 < 0) return;
+    const int U = min(recv_offsets[rank + 1] - r0, g.T * g.k - r0);
+    const int base = expert_offsets[rank * g.E_loc];
+    const int rows_r = min(expert_offsets[(rank + 1) * g.E_loc] - base, out_rows);
+    const int items = U * pieces;
+    const int lane = lane_id();
+    const int nwaves = gridDim.x * kWavesPerBlock;
+    for (int it = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < items; it += nwaves) {
+        const int u = it / pieces;
+        const int t = recv_token[r0 + u];
+        if (static_cast<unsigned>(t) >= static_cast<unsigned>(g.T)) continue;
+        int row = -1;
+        if (lane < g.k) {
+            const int rr = slot_pos[static_cast<size_t>(t) * g.k + lane] - base;
+            row = static_cast<unsigned>(rr) < static_cast<unsigned>(rows_r) ? rr : -1;
+        }
+        int rows[kMaxK];
+        const int n = compact_rows(row, rows);
+        fan_out<JB>(x + static_cast<size_t>(t) * vpr, out, vpr, row_piece(vpr, pieces, it - u * pieces), n, rows);
+    }
+}
+
+// ---------------------------------------------------------------- send pack
+template <int JB>
+__global__ __launch_bounds__(kThreads) void send_pack_kernel(
+    Topo g, int src_rank, int vpr, int pieces, const u32x4* __restrict__ x, const int32_t* __restrict__ idx,
+    const uint8_t* __restrict__ keep, const int32_t* __restrict__ er, const uint64_t* __restrict__ mask,
+    const int32_t* __restrict__ copy_row, const int32_t* __restrict__ send_counts,
+    const int32_t* __restrict__ send_offsets, u32x4* __restrict__ out, int out_rows) {
+    __shared__ int32_t dev_of[kMaxE];
+    __shared__ int32_t row0[kMaxR];   // send_offsets[s][d] - (rows of d from sources < s)
+    __shared__ int32_t total_lds;
+    for (int e = threadIdx.x; e < g.E; e += kThreads) dev_of[e] = er[e];
+    if (threadIdx.x < g.R) row0[threadIdx.x] = send_offsets[src_rank * g.R + threadIdx.x];
+    if (threadIdx.x == 0) total_lds = 0;
+    __syncthreads();
+    for (int j = threadIdx.x; j < src_rank * g.R; j += kThreads) atomicSub(&row0[j % g.R], send_counts[j]);
+    if (threadIdx.x < g.R) atomicAdd(&total_lds, send_counts[src_rank * g.R + threadIdx.x]);
+    __syncthreads();
+    const int total = min(total_lds, out_rows);
+    const int lane = lane_id();
+    const int items = g.tpr * pieces;
+    const int nwaves = gridDim.x * kWavesPerBlock;
+    for (int it = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < items; it += nwaves) {
+        const int i = it / pieces;
+        const int t = src_rank * g.tpr + i;
+        const uint64_t m = mask[t];
+        int d = -1, cr = -1;
+        if (lane < g.k) {
+            const size_t q = static_cast<size_t>(t) * g.k + lane;
+            const int e = idx[q];
+            if (keep[q] && static_cast<unsigned>(e) < static_cast<unsigned>(g.E)) d = dev_of[e];
+            cr = copy_row[q];
+            if (static_cast<unsigned>(d) >= static_cast<unsigned>(g.R) || !((m >> d) & 1ull)) d = -1;
+        }
+        // one row per device: the device's first kept slot writes it
+        bool first = d >= 0;
+#pragma unroll
+        for (int s2 = 0; s2 < kMaxK; ++s2) {
+            const int d2 = __shfl(d, s2);
+            if (s2 < lane && d2 == d) first = false;
+        }
+        int row = -1;
+        if (first) {
+            const int rr = row0[d] + cr;
+            row = static_cast<unsigned>(rr) < static_cast<unsigned>(total) ? rr : -1;
+        }
+        int rows[kMaxK];
+        const int n = compact_rows(row, rows);
+        fan_out<JB>(x + static_cast<size_t>(t) * vpr, out, vpr, row_piece(vpr, pieces, it - i * pieces), n, rows);
+    }
+}
+
+// ---------------------------------------------------------------- dest reduce
+template <typename RowT, int JB>
+__global__ __launch_bounds__(kThreads) void dest_reduce_kernel(
+    Topo g, int rank, int vpr, int pieces, const u32x4* __restrict__ Y, const float* __restrict__ w,
+    const int32_t* __restrict__ slot_pos, const int32_t* __restrict__ expert_offsets,
+    const int32_t* __restrict__ recv_offsets, const int32_t* __restrict__ recv_token,
+    u32x4* __restrict__ out, int in_rows, int out_rows) {
+    const int r0 = recv_offsets[rank];
+    if (r0 < 0) return;
     const int U = min(min(recv_offsets[rank + 1] - r0, g.T * g.k - r0), out_rows - r0);
     const int base = expert_offsets[rank * g.E_loc];
     const int rows_r = min(expert_offsets[(rank + 1) * g.E_loc] - base, in_rows);
-    if (r0 < 0) return;
+    const int items = U * pieces;
+    const int lane = lane_id();
     const int nwaves = gridDim.x * kWavesPerBlock;
-    for (int u = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; u < U; u += nwaves) {
+    for (int it = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < items; it += nwaves) {
+        const int u = it / pieces;
         const int t = recv_token[r0 + u];
-        int row[kMaxK];
-        float wt[kMaxK];
-#pragma unroll
-        for (int s = 0; s < kMaxK; ++s) {
-            row[s] = -1;
-            wt[s] = 0.0f;
-            if (s < g.k && static_cast<unsigned>(t) < static_cast<unsigned>(g.T)) {
-                const size_t q = static_cast<size_t>(t) * g.k + s;
-                if (keep[q] && expert_rank_of(er, idx[q], g) == rank) {
-                    const int rr = slot_pos[q] - base;
-                    if (static_cast<unsigned>(rr) < static_cast<unsigned>(rows_r)) { row[s] = rr; wt[s] = w[q]; }
-                }
+        int row = -1;
+        float wl = 0.0f;
+        if (lane < g.k && static_cast<unsigned>(t) < static_cast<unsigned>(g.T)) {
+            const size_t q = static_cast<size_t>(t) * g.k + lane;
+            const int rr = slot_pos[q] - base;
+            if (static_cast<unsigned>(rr) < static_cast<unsigned>(rows_r)) {
+                row = rr;
+                wl = w[q];
             }
         }
-        V* dst = out + static_cast<size_t>(r0 + u) * vec_per_row;
-        for (int c = lane_id(); c < vec_per_row; c += kWave) {
-            float acc[RowT::kElems];
+        // slot-ordered list of (row, weight)
+        uint64_t vb = __ballot(row >= 0);
+        const int n = __popcll(vb);
+        int rows[kMaxK];
+        float wt[kMaxK];
 #pragma unroll
-            for (int i = 0; i < RowT::kElems; ++i) acc[i] = 0.0f;
-#pragma unroll
-            for (int s = 0; s < kMaxK; ++s) {
-                if (row[s] < 0) continue;
-                float f[RowT::kElems];
-                RowT::load(Y[static_cast<size_t>(row[s]) * vec_per_row + c], f);
-#pragma unroll
-                for (int i = 0; i < RowT::kElems; ++i) acc[i] = __builtin_fmaf(wt[s], f[i], acc[i]);
+        for (int j = 0; j < kMaxK; ++j) {
+            rows[j] = 0;
+            wt[j] = 0.0f;
+            if (j < n) {
+                const int s = __ffsll(static_cast<unsigned long long>(vb)) - 1;
+                rows[j] = __builtin_amdgcn_readlane(row, s);
+                wt[j] = lane_value(wl, s);
+                vb &= vb - 1;
             }
-            dst[c] = RowT::store(acc);
+        }
+        const Piece pc = row_piece(vpr, pieces, it - u * pieces);
+        u32x4* dst = out + static_cast<size_t>(r0 + u) * vpr;
+        for (int c0 = pc.begin + lane; c0 < pc.end; c0 += kWave * JB) {
+            u32x4 v[kMaxK][JB];
+#pragma unroll
+            for (int r = 0; r < kMaxK; ++r) {
+                if (r >= n) break;
+                const u32x4* src = Y + static_cast<size_t>(rows[r]) * vpr;
+#pragma unroll
+                for (int j = 0; j < JB; ++j) {
+                    const int c = c0 + j * kWave;
+                    if (c < pc.end) v[r][j] = src[c];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int c = c0 + j * kWave;
+                float acc[RowT::kElems];
+#pragma unroll
+                for (int e = 0; e < RowT::kElems; ++e) acc[e] = 0.0f;
+#pragma unroll
+                for (int r = 0; r < kMaxK; ++r) {
+                    if (r >= n) break;
+                    float f[RowT::kElems];
+                    RowT::load(v[r][j], f);
+#pragma unroll
+                    for (int e = 0; e < RowT::kElems; ++e) acc[e] = __builtin_fmaf(wt[r], f[e], acc[e]);
+                }
+                if (c < pc.end) dst[c] = RowT::store(acc);
+            }
         }
     }
 }
 
 // ---------------------------------------------------------------- src reduce
-template <typename RowT>
+template <typename RowT, int JB>
 __global__ __launch_bounds__(kThreads) void src_reduce_kernel(
-    Topo g, int src_rank, int vec_per_row, const typename RowT::V* __restrict__ parts,
+    Topo g, int src_rank, int vpr, int pieces, const u32x4* __restrict__ parts,
     const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep, const int32_t* __restrict__ er,
     const uint64_t* __restrict__ mask, const int32_t* __restrict__ copy_row,
-    const int32_t* __restrict__ recv_offsets, const typename RowT::V* __restrict__ shared,
-    typename RowT::V* __restrict__ out, int in_rows) {
-    typedef typename RowT::V V;
-    const int total = min(recv_offsets[g.R], in_rows);
+    const int32_t* __restrict__ recv_offsets, const u32x4* __restrict__ shared,
+    u32x4* __restrict__ out, int in_rows) {
+    __shared__ int32_t dev_of[kMaxE];
+    __shared__ int32_t roff[kMaxR + 1];
+    for (int e = threadIdx.x; e < g.E; e += kThreads) dev_of[e] = er[e];
+    if (threadIdx.x <= g.R) roff[threadIdx.x] = recv_offsets[threadIdx.x];
+    __syncthreads();
+    const int total = min(roff[g.R], in_rows);
+    const int lane = lane_id();
+    const int items = g.tpr * pieces;
     const int nwaves = gridDim.x * kWavesPerBlock;
-    for (int i = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; i < g.tpr; i += nwaves) {
+    for (int it = blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; it < items; it += nwaves) {
+        const int i = it / pieces;
         const int t = src_rank * g.tpr + i;
         const uint64_t m = mask[t];
-        // one returned row per kept device, ascending device id
-        int rows[kMaxK];
-        int n = 0;
-        for (int d = 0; d < g.R && n < kMaxK; ++d) {
-            if (!((m >> d) & 1ull)) continue;
-            int cr = -1;
-            for (int s = 0; s < g.k; ++s) {
-                const size_t q = static_cast<size_t>(t) * g.k + s;
-                if (cr < 0 && keep[q] && expert_rank_of(er, idx[q], g) == d) cr = copy_row[q];
-            }
-            const int row = recv_offsets[d] + cr;
-            if (cr >= 0 && row >= 0 && row < total) rows[n++] = row;
+        int d = -1, cr = -1;
+        if (lane < g.k) {
+            const size_t q = static_cast<size_t>(t) * g.k + lane;
+            const int e = idx[q];
+            cr = copy_row[q];
+            if (keep[q] && static_cast<unsigned>(e) < static_cast<unsigned>(g.E)) d = dev_of[e];
+            if (static_cast<unsigned>(d) >= static_cast<unsigned>(g.R) || !((m >> d) & 1ull) || cr < 0) d = -1;
         }
-        V* dst = out + static_cast<size_t>(i) * vec_per_row;
-        for (int c = lane_id(); c < vec_per_row; c += kWave) {
-            float acc[RowT::kElems];
-            if (shared) {
-                RowT::load(shared[static_cast<size_t>(i) * vec_per_row + c], acc);
-            } else {
+        // one returned row per kept device (its first kept slot), ascending device
+        bool first = d >= 0;
 #pragma unroll
-                for (int j = 0; j < RowT::kElems; ++j) acc[j] = 0.0f;
-            }
-            for (int j = 0; j < n; ++j) {
-                float f[RowT::kElems];
-                RowT::load(parts[static_cast<size_t>(rows[j]) * vec_per_row + c], f);
+        for (int s2 = 0; s2 < kMaxK; ++s2) {
+            const int d2 = __shfl(d, s2);
+            if (s2 < lane && d2 == d) first = false;
+        }
+        int row = -1;
+        if (first) {
+            const int rr = roff[d] + cr;
+            row = (rr >= 0 && rr < total) ? rr : -1;
+        }
+        int ord = 0;   // place of this lane's device among the valid devices
 #pragma unroll
-                for (int e = 0; e < RowT::kElems; ++e) acc[e] += f[e];
+        for (int s2 = 0; s2 < kMaxK; ++s2) {
+            const int d2 = __shfl(d, s2);
+            const int row2 = __shfl(row, s2);
+            if (row2 >= 0 && d2 < d) ++ord;
+        }
+        const uint64_t valid = __ballot(row >= 0);
+        const int n = __popcll(valid);
+        int rows[kMaxK];
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j) {
+            rows[j] = 0;
+            if (j < n) {
+                // ords of the valid lanes are distinct, so exactly one lane answers
+                const uint64_t at = __ballot(row >= 0 && ord == j);
+                rows[j] = at ? __builtin_amdgcn_readlane(row, __ffsll(static_cast<unsigned long long>(at)) - 1) : 0;
             }
-            dst[c] = RowT::store(acc);
+        }
+        const Piece pc = row_piece(vpr, pieces, it - i * pieces);
+        const size_t orow = static_cast<size_t>(i) * vpr;
+        for (int c0 = pc.begin + lane; c0 < pc.end; c0 += kWave * JB) {
+            u32x4 v[kMaxK + 1][JB];
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int c = c0 + j * kWave;
+                if (shared && c < pc.end) v[kMaxK][j] = shared[orow + c];
+            }
+#pragma unroll
+            for (int r = 0; r < kMaxK; ++r) {
+                if (r >= n) break;
+                const u32x4* src = parts + static_cast<size_t>(rows[r]) * vpr;
+#pragma unroll
+                for (int j = 0; j < JB; ++j) {
+                    const int c = c0 + j * kWave;
+                    if (c < pc.end) v[r][j] = src[c];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < JB; ++j) {
+                const int c = c0 + j * kWave;
+                float acc[RowT::kElems];
+                if (shared) {
+                    RowT::load(v[kMaxK][j], acc);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < RowT::kElems; ++e) acc[e] = 0.0f;
+                }
+#pragma unroll
+                for (int r = 0; r < kMaxK; ++r) {
+                    if (r >= n) break;
+                    float f[RowT::kElems];
+                    RowT::load(v[r][j], f);
+#pragma unroll
+                    for (int e = 0; e < RowT::kElems; ++e) acc[e] += f[e];
+                }
+                if (c < pc.end) out[orow + c] = RowT::store(acc);
+            }
         }
     }
 }
@@ -251,8 +395,16 @@ Topo make_topo(const cap_topology* tp) {
     return g;
 }
 
-int row_grid(long long rows_upper) {
-    const long long need = (rows_upper + kWavesPerBlock - 1) / kWavesPerBlock;
+// Pieces per row: split rows (in whole 64-lane chunk groups) only when the
+// rows alone would leave the chip short of waves.
+int row_pieces(long long rows_upper, int vpr) {
+    int p = 1;
+    while (p < 4 && rows_upper * p < kTargetWaves && vpr >= 2 * p * kWave) p *= 2;
+    return p;
+}
+
+int row_grid(long long items_upper) {
+    const long long need = (items_upper + kWavesPerBlock - 1) / kWavesPerBlock;
     const long long cap = static_cast<long long>(device_cu_count()) * 8;
     return static_cast<int>(need < 1 ? 1 : (need < cap ? need : cap));
 }
@@ -265,14 +417,18 @@ cap_status permute_launch(const cap_topology* tp, cap_permute_mode mode, int ran
     const Topo g = make_topo(tp);
     const int row_bytes = d * (dt == CAP_DTYPE_BF16 ? 2 : 4);
     const int vpr = row_bytes / 16;
+    const u32x4* xv = static_cast<const u32x4*>(x);
+    u32x4* ov = static_cast<u32x4*>(out);
     if (mode == CAP_PERMUTE_EXPERT_GATHER) {
-        expert_gather_kernel<uint4><<<row_grid(g.T), kThreads, 0, st>>>(
-            g, rank, vpr, static_cast<const uint4*>(x), idx, keep, tp->expert_rank, lay->slot_pos,
-            lay->expert_offsets, lay->recv_offsets, lay->recv_token, static_cast<uint4*>(out), out_rows);
+        const int pieces = row_pieces(g.T, vpr);
+        expert_gather_kernel<4><<<row_grid(static_cast<long long>(g.T) * pieces), kThreads, 0, st>>>(
+            g, rank, vpr, pieces, xv, lay->slot_pos, lay->expert_offsets, lay->recv_offsets, lay->recv_token,
+            ov, out_rows);
     } else {
-        send_pack_kernel<uint4><<<row_grid(g.tpr), kThreads, 0, st>>>(
-            g, rank, vpr, static_cast<const uint4*>(x), idx, keep, tp->expert_rank, mask, lay->copy_row,
-            lay->send_counts, lay->send_offsets, static_cast<uint4*>(out), out_rows);
+        const int pieces = row_pieces(g.tpr, vpr);
+        send_pack_kernel<4><<<row_grid(static_cast<long long>(g.tpr) * pieces), kThreads, 0, st>>>(
+            g, rank, vpr, pieces, xv, idx, keep, tp->expert_rank, mask, lay->copy_row, lay->send_counts,
+            lay->send_offsets, ov, out_rows);
     }
     CAP_LAUNCH_CHECK();
     return CAP_OK;
@@ -283,26 +439,32 @@ cap_status combine_launch(const cap_topology* tp, cap_combine_mode mode, int ran
                           const uint64_t* mask, const cap_layout* lay, const void* shared_out, void* out,
                           int out_rows, hipStream_t st) {
     const Topo g = make_topo(tp);
+    const int vpr = d * (dt == CAP_DTYPE_BF16 ? 2 : 4) / 16;
+    const u32x4* iv = static_cast<const u32x4*>(in);
+    const u32x4* sv = static_cast<const u32x4*>(shared_out);
+    u32x4* ov = static_cast<u32x4*>(out);
     if (mode == CAP_COMBINE_DEST_REDUCE) {
-        if (dt == CAP_DTYPE_BF16) {
-            dest_reduce_kernel<Bf16Row><<<row_grid(g.T), kThreads, 0, st>>>(
-                g, rank, d / 8, static_cast<const uint4*>(in), idx, w, keep, tp->expert_rank, lay->slot_pos,
-                lay->expert_offsets, lay->recv_offsets, lay->recv_token, static_cast<uint4*>(out), in_rows, out_rows);
-        } else {
-            dest_reduce_kernel<F32Row><<<row_grid(g.T), kThreads, 0, st>>>(
-                g, rank, d / 4, static_cast<const float4*>(in), idx, w, keep, tp->expert_rank, lay->slot_pos,
-                lay->expert_offsets, lay->recv_offsets, lay->recv_token, static_cast<float4*>(out), in_rows, out_rows);
-        }
+        const int pieces = row_pieces(g.T, vpr);
+        const int grid = row_grid(static_cast<long long>(g.T) * pieces);
+        if (dt == CAP_DTYPE_BF16)
+            dest_reduce_kernel<Bf16Row, 2><<<grid, kThreads, 0, st>>>(
+                g, rank, vpr, pieces, iv, w, lay->slot_pos, lay->expert_offsets, lay->recv_offsets,
+                lay->recv_token, ov, in_rows, out_rows);
+        else
+            dest_reduce_kernel<F32Row, 2><<<grid, kThreads, 0, st>>>(
+                g, rank, vpr, pieces, iv, w, lay->slot_pos, lay->expert_offsets, lay->recv_offsets,
+                lay->recv_token, ov, in_rows, out_rows);
     } else {
-        if (dt == CAP_DTYPE_BF16) {
-            src_reduce_kernel<Bf16Row><<<row_grid(g.tpr), kThreads, 0, st>>>(
-                g, rank, d / 8, static_cast<const uint4*>(in), idx, keep, tp->expert_rank, mask, lay->copy_row,
-                lay->recv_offsets, static_cast<const uint4*>(shared_out), static_cast<uint4*>(out), in_rows);
-        } else {
-            src_reduce_kernel<F32Row><<<row_grid(g.tpr), kThreads, 0, st>>>(
-                g, rank, d / 4, static_cast<const float4*>(in), idx, keep, tp->expert_rank, mask, lay->copy_row,
-                lay->recv_offsets, static_cast<const float4*>(shared_out), static_cast<float4*>(out), in_rows);
-        }
+        const int pieces = row_pieces(g.tpr, vpr);
+        const int grid = row_grid(static_cast<long long>(g.tpr) * pieces);
+        if (dt == CAP_DTYPE_BF16)
+            src_reduce_kernel<Bf16Row, 2><<<grid, kThreads, 0, st>>>(
+                g, rank, vpr, pieces, iv, idx, keep, tp->expert_rank, mask, lay->copy_row, lay->recv_offsets,
+                sv, ov, in_rows);
+        else
+            src_reduce_kernel<F32Row, 2><<<grid, kThreads, 0, st>>>(
+                g, rank, vpr, pieces, iv, idx, keep, tp->expert_rank, mask, lay->copy_row, lay->recv_offsets,
+                sv, ov, in_rows);
     }
     CAP_LAUNCH_CHECK();
     return CAP_OK;
