@@ -145,7 +145,7 @@ int32_t cap_version(void);
 
 /*
  * Workspace bytes that `op` needs for this topology and shape (0 if none).
- *   CAP_OP_DISPATCH_LAYOUT: per-chunk partial counts (uses topo only).
+ *   CAP_OP_DISPATCH_LAYOUT: per-chunk column counts, column totals and volume sums (uses topo only).
  *   CAP_OP_EXPERT_FFN: the SwiGLU intermediate H, max_rows x inter values of
  *                      `dtype` (topo and d unused, may be NULL / 0).
  *   CAP_OP_COACTIVATION: per-split partial counts (uses topo->T and topo->E).

@@ -31,9 +31,17 @@ CXXFLAGS = [
 ]
 
 
+# Per-file additions.  route_prune: its inputs are finite by contract, and
+# without NaN semantics the instruction selector does not re-derive NaN facts
+# through the long compare/select networks of the top-k (minutes -> seconds).
+FILE_FLAGS = {
+    "route_prune.hip": ["-fno-honor-nans"],
+}
+
+
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD, os.path.basename(src).replace(".hip", ".o"))
-    cmd = [HIPCC, *CXXFLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *CXXFLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -9,19 +9,30 @@
 // order, with no contraction, so the decision is reproducible bit for bit:
 //   gates  w_s = q_s / S, q_s = gate_exp(l_s - l_0), S = ((q_0 + q_1) + ...)
 //   a_d    = sum of w_s on device d in slot order
-//   key_d  = +inf (own device), a_d / 1 (same node), a_d / c (other node)
+//   key_d  = +inf (own device), a_d (same node), a_d / c (other node)
 //   greedy running sum in key order (ties: lower device id), stop at >= 1 - p
 //   w'_s   = w_s / S' over kept slots (S' summed in slot order).
 //
-// Layout: 8 lanes cooperate on one token (8 tokens per wave).  Lane j of a
-// group holds V logits of the row, loaded as 16-byte vectors so a group reads
-// the row in contiguous 128-byte pieces.  Each lane keeps a sorted top-KI list
-// of its own values (stable: it scans its values in ascending expert order and
-// inserts only on strictly greater), then three butterfly steps (xor 1, 2, 4)
-// merge partner lists with a bitonic network under the total order
-// (value desc, index asc).  After the merge all 8 lanes hold the token's
-// top-KI list, compute the gates and the pruning redundantly (uniform work, no
-// divergence) and lane j writes slot j.
+// Selection keys.  A (logit, expert) pair is packed into one positive fp64
+// whose order is the selection order (logit descending, then expert id
+// ascending): bits 61..30 hold the logit's order-preserving 32-bit image and
+// bits 7..0 hold 255 - expert.  Such a double is never NaN or infinite and,
+// for every finite logit, is a normal number, so v_max_f64 / v_min_f64 compare
+// it exactly; a compare-exchange is then two branch-free instructions.  -0.0
+// is folded to +0.0 first, because the two compare equal as logits (the tie
+// then goes to the lower expert id, as for any other equal pair).
+//
+// Layout: 8 lanes cooperate on one token (8 tokens per wave).  Lane j holds V
+// logits of the row (loaded as 16-byte vectors, so a group reads the row in
+// contiguous 128-byte pieces), sorts them in blocks of KP = pow2 >= k with a
+// bitonic network and keeps the top KP; three butterfly merges across the
+// group (DPP lane swaps) leave every lane with the token's sorted top KP.
+// From there lane j owns slot j: it computes its own gate exponential and
+// takes the slot-ordered sums (S, a_d, S') from the group's lanes through
+// ds_swizzle broadcasts, so every sum keeps its sequential order.  The
+// candidate devices (one lane each) are sorted across the group with the same
+// packed-double network, and each lane replays the greedy over the sorted
+// list to build the device mask.
 #pragma clang fp contract(off)
 
 #include <math.h>
@@ -33,6 +44,7 @@ namespace {
 
 constexpr int kGroup = 8;              // lanes per token
 constexpr int kTokensPerBlock = 32;    // 256 threads
+constexpr double kNoKey = -1.0;        // below every packed key
 
 // Gate exponential: Cody & Waite argument reduction with ln2 split as
 // LN2_HI (ln 2 to 16 significant bits, exact products n*LN2_HI for |n| < 2^8)
@@ -40,7 +52,6 @@ constexpr int kTokensPerBlock = 32;    // 256 threads
 // with fp32(1/j!) coefficients by Horner with fused multiply-add; scaled by
 // 2^n.  Inputs below -87.33 give 0, so results are never subnormal.
 __device__ __forceinline__ float gate_exp(float z) {
-    if (!(z >= -87.33f)) return 0.0f;
     const float n = __builtin_rintf(z * 1.44269504088896340736f);
     float r = __builtin_fmaf(-n, 0.693145751953125f, z);
     r = __builtin_fmaf(-n, 1.42860682030941723212e-6f, r);
@@ -52,242 +63,308 @@ __device__ __forceinline__ float gate_exp(float z) {
     q = __builtin_fmaf(q, r, 0.5f);
     q = __builtin_fmaf(q, r, 1.0f);
     q = __builtin_fmaf(q, r, 1.0f);
-    return __builtin_ldexpf(q, static_cast<int>(n));
+    const float e = __builtin_ldexpf(q, static_cast<int>(n));
+    return (z >= -87.33f) ? e : 0.0f;
 }
 
-// (value desc, index asc): true if (av, ai) ranks before (bv, bi).
-__device__ __forceinline__ bool ranks_before(float av, int ai, float bv, int bi) {
-    return av > bv || (av == bv && ai < bi);
+// Order-preserving image of a float (total order on non-NaN values).
+__device__ __forceinline__ uint32_t ordered_bits(float x) {
+    const uint32_t b = __float_as_uint(x + 0.0f);   // -0.0 -> +0.0
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float from_ordered_bits(uint32_t u) {
+    return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
 }
 
-template <int V, int KI>
+__device__ __forceinline__ double pack_key(float x, int e) {
+    const uint64_t k = (static_cast<uint64_t>(ordered_bits(x)) << 30) | static_cast<uint64_t>(255 - e);
+    return __longlong_as_double(static_cast<long long>(k));
+}
+__device__ __forceinline__ int key_expert(double k) {
+    return 255 - static_cast<int>(static_cast<uint64_t>(__double_as_longlong(k)) & 255u);
+}
+__device__ __forceinline__ float key_logit(double k) {
+    return from_ordered_bits(static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(k)) >> 30));
+}
+
+// Descending compare-exchange.
+__device__ __forceinline__ void cx(double& a, double& b) {
+    const double hi = __builtin_fmax(a, b);
+    const double lo = __builtin_fmin(a, b);
+    a = hi;
+    b = lo;
+}
+
+// Bitonic sort (descending) of N = 2^m keys.
+template <int N>
+__device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
+#pragma unroll
+    for (int size = 2; size <= N; size <<= 1) {
+#pragma unroll
+        for (int stride = size / 2; stride >= 1; stride >>= 1) {
+#pragma unroll
+            for (int i = 0; i < N; ++i) {
+                const int j = i ^ stride;
+                if (j > i) {
+                    // descending within blocks whose (i & size) == 0, ascending otherwise
+                    if ((i & size) == 0) cx(v[i], v[j]);
+                    else cx(v[j], v[i]);
+                }
+            }
+        }
+    }
+}
+
+// a := top N of (a, b), both sorted descending; result sorted descending.
+template <int N>
+__device__ __forceinline__ void merge_top(double (&a)[N], const double (&b)[N]) {
+#pragma unroll
+    for (int s = 0; s < N; ++s) a[s] = __builtin_fmax(a[s], b[N - 1 - s]);   // bitonic
+#pragma unroll
+    for (int stride = N / 2; stride >= 1; stride >>= 1)
+#pragma unroll
+        for (int i = 0; i < N; ++i)
+            if ((i & stride) == 0) cx(a[i], a[i + stride]);
+}
+
+// Lane swaps inside a group of 8 lanes (DPP): xor 1, xor 2 (quad permutes)
+// and the mirror i <-> 7 - i (the third merge only needs each lane of one
+// half paired with a lane of the other half).
+template <int CTRL>
+__device__ __forceinline__ double dpp_swap(double v) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(b), CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(b >> 32), CTRL, 0xF, 0xF, false);
+    return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<uint32_t>(lo));
+}
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // row_half_mirror
+
+template <int CTRL, int N>
+__device__ __forceinline__ void merge_with_partner(double (&a)[N]) {
+    double b[N];
+#pragma unroll
+    for (int s = 0; s < N; ++s) b[s] = dpp_swap<CTRL>(a[s]);
+    merge_top<N>(a, b);
+}
+
+constexpr int pow2_at_least(int k) { return k <= 1 ? 1 : k <= 2 ? 2 : k <= 4 ? 4 : 8; }
+
+// Value of lane s of the caller's 8-lane group (ds_swizzle, bit-mask mode:
+// lane = (lane & 0b11000) | s within each 32-lane half).
+template <int S>
+__device__ __forceinline__ int group_lane(int v) {
+    return __builtin_amdgcn_ds_swizzle(v, 0x18 | (S << 5));
+}
+template <int S>
+__device__ __forceinline__ float group_lane(float v) {
+    return __int_as_float(group_lane<S>(__float_as_int(v)));
+}
+
+// One step of a descending sort across the 8 lanes: the lane that is `lower`
+// in its pair keeps the larger (key, a), the other keeps the smaller.
+template <int CTRL>
+__device__ __forceinline__ void lane_cx(double& key, float& a, bool lower) {
+    const double pk = dpp_swap<CTRL>(key);
+    const float pa = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), CTRL, 0xF, 0xF, false));
+    const bool take = lower ? (pk > key) : (pk < key);
+    key = take ? pk : key;
+    a = take ? pa : a;
+}
+constexpr int kDppMirror4 = 0x1B;       // quad_perm [3,2,1,0]
+
+template <int V, int K, bool VEC>
 __global__ __launch_bounds__(256) void route_prune_kernel(
-    const float* __restrict__ logits, int T, int E, int k, int R, int ranks_per_node,
-    int tokens_per_rank, float inter_node_cost, float p, int vec_ok,
+    const float* __restrict__ logits, int T, int E, int R, int ranks_per_node,
+    int tokens_per_rank, float inter_node_cost, float p,
     const int32_t* __restrict__ expert_rank, int32_t* __restrict__ out_idx,
     float* __restrict__ out_w, uint8_t* __restrict__ out_keep, uint64_t* __restrict__ out_mask) {
+    constexpr int KP = pow2_at_least(K);
     __shared__ int er_lds[kMaxE];
     for (int e = threadIdx.x; e < E; e += blockDim.x) er_lds[e] = expert_rank[e] & 63;
-    __syncthreads();
 
     const int g = threadIdx.x & (kGroup - 1);
     const int t = blockIdx.x * kTokensPerBlock + (threadIdx.x >> 3);
     const bool live = t < T;
     const float* row = logits + static_cast<size_t>(live ? t : T - 1) * E;
 
-    // ---- load this lane's V values; element order ascending within the lane
+    // ---- this lane's V logits; lane g owns columns c*(8*CW) + g*CW + [0, CW)
     constexpr int CW = V < 4 ? V : 4;          // vector width
     float vals[V];
-    int ids[V];
+    if constexpr (VEC) {
 #pragma unroll
-    for (int c = 0; c < V / CW; ++c) {
-        const int e0 = c * (kGroup * CW) + g * CW;
-        if (vec_ok) {
+        for (int c = 0; c < V / CW; ++c) {
+            const int e0 = c * (kGroup * CW) + g * CW;
             if constexpr (CW == 4) {
-                const float4 v = *reinterpret_cast<const float4*>(row + e0);
-                vals[c * 4 + 0] = v.x; vals[c * 4 + 1] = v.y; vals[c * 4 + 2] = v.z; vals[c * 4 + 3] = v.w;
+                const float4 q = *reinterpret_cast<const float4*>(row + e0);
+                vals[c * 4 + 0] = q.x; vals[c * 4 + 1] = q.y; vals[c * 4 + 2] = q.z; vals[c * 4 + 3] = q.w;
             } else if constexpr (CW == 2) {
-                const float2 v = *reinterpret_cast<const float2*>(row + e0);
-                vals[c * 2 + 0] = v.x; vals[c * 2 + 1] = v.y;
+                const float2 q = *reinterpret_cast<const float2*>(row + e0);
+                vals[c * 2 + 0] = q.x; vals[c * 2 + 1] = q.y;
             } else {
                 vals[c] = row[e0];
             }
-        } else {
-#pragma unroll
-            for (int i = 0; i < CW; ++i) vals[c * CW + i] = (e0 + i < E) ? row[e0 + i] : -INFINITY;
         }
+    } else {
 #pragma unroll
-        for (int i = 0; i < CW; ++i) ids[c * CW + i] = e0 + i;
-    }
-
-    // ---- lane-local sorted top-KI (stable insertion on strictly greater)
-    float lv[KI];
-    int li[KI];
+        for (int c = 0; c < V / CW; ++c)
 #pragma unroll
-    for (int s = 0; s < KI; ++s) { lv[s] = -INFINITY; li[s] = 0x7fffffff; }
-#pragma unroll
-    for (int i = 0; i < V; ++i) {
-        const float x = vals[i];
-        const int xe = ids[i];
-        bool gt[KI];
-#pragma unroll
-        for (int s = 0; s < KI; ++s) gt[s] = x > lv[s];
-#pragma unroll
-        for (int s = KI - 1; s >= 1; --s) {
-            lv[s] = gt[s - 1] ? lv[s - 1] : (gt[s] ? x : lv[s]);
-            li[s] = gt[s - 1] ? li[s - 1] : (gt[s] ? xe : li[s]);
-        }
-        lv[0] = gt[0] ? x : lv[0];
-        li[0] = gt[0] ? xe : li[0];
-    }
-
-    // ---- butterfly merge of the 8 lane lists (bitonic, total order)
-#pragma unroll
-    for (int m = 1; m < kGroup; m <<= 1) {
-        float ov[KI];
-        int oi[KI];
-#pragma unroll
-        for (int s = 0; s < KI; ++s) {
-            ov[s] = __shfl_xor(lv[s], m);
-            oi[s] = __shfl_xor(li[s], m);
-        }
-        float cv[KI];
-        int ci[KI];
-#pragma unroll
-        for (int s = 0; s < KI; ++s) {
-            const bool mine = ranks_before(lv[s], li[s], ov[KI - 1 - s], oi[KI - 1 - s]);
-            cv[s] = mine ? lv[s] : ov[KI - 1 - s];
-            ci[s] = mine ? li[s] : oi[KI - 1 - s];
-        }
-#pragma unroll
-        for (int h = KI / 2; h >= 1; h >>= 1) {
-#pragma unroll
-            for (int s = 0; s < KI; ++s) {
-                if ((s & h) == 0) {
-                    const bool swap = ranks_before(cv[s + h], ci[s + h], cv[s], ci[s]);
-                    const float tv = cv[s];
-                    const int ti = ci[s];
-                    cv[s] = swap ? cv[s + h] : cv[s];
-                    ci[s] = swap ? ci[s + h] : ci[s];
-                    cv[s + h] = swap ? tv : cv[s + h];
-                    ci[s + h] = swap ? ti : ci[s + h];
-                }
+            for (int i = 0; i < CW; ++i) {
+                const int e = c * (kGroup * CW) + g * CW + i;
+                vals[c * CW + i] = row[e < E ? e : E - 1];
             }
-        }
-#pragma unroll
-        for (int s = 0; s < KI; ++s) { lv[s] = cv[s]; li[s] = ci[s]; }
     }
+    double keys[V];
+#pragma unroll
+    for (int c = 0; c < V / CW; ++c)
+#pragma unroll
+        for (int i = 0; i < CW; ++i) {
+            const int e = c * (kGroup * CW) + g * CW + i;
+            keys[c * CW + i] = (VEC || e < E) ? pack_key(vals[c * CW + i], e) : kNoKey;
+        }
+    __syncthreads();                           // er_lds ready (the loads are in flight)
 
-    // ---- normalised gates (softmax over the k selected logits)
-    float w[KI];
+    // ---- lane-local top KP: sort blocks of KP keys, merge them
+    double top[KP];
+    {
+        constexpr int B = V < KP ? V : KP;     // keys per block
+#pragma unroll
+        for (int s = 0; s < KP; ++s) top[s] = s < B ? keys[s] : kNoKey;
+        bitonic_sort<KP>(top);
+#pragma unroll
+        for (int b0 = KP; b0 < V; b0 += KP) {
+            double blk[KP];
+#pragma unroll
+            for (int s = 0; s < KP; ++s) blk[s] = keys[b0 + s];
+            bitonic_sort<KP>(blk);
+            merge_top<KP>(top, blk);
+        }
+    }
+    // ---- merge across the 8 lanes of the token
+    merge_with_partner<kDppXor1, KP>(top);
+    merge_with_partner<kDppXor2, KP>(top);
+    merge_with_partner<kDppHalfMirror, KP>(top);
+
+    // ---- lane g owns slot g (lanes g >= K own nothing)
+    double mine = top[0];
+#pragma unroll
+    for (int s = 1; s < KP; ++s) mine = (g == s) ? top[s] : mine;
+    const bool has_slot = g < K;
+    const int my_e = key_expert(mine);
+    const int my_dev = has_slot ? er_lds[my_e < E ? my_e : 0] : -1;
+
+    // gates: q_g = gate_exp(l_g - l_0); S = ((q_0 + q_1) + ...) in slot order
+    const float q = has_slot ? gate_exp(key_logit(mine) - key_logit(top[0])) : 0.0f;
+    float qs[K];
+    int devs[K];
+#define CAP_GATHER_SLOT(S_)                                  \
+    if constexpr (S_ < K) {                                  \
+        qs[S_] = group_lane<S_>(q);                          \
+        devs[S_] = group_lane<S_>(my_dev);                   \
+    }
+    CAP_GATHER_SLOT(0) CAP_GATHER_SLOT(1) CAP_GATHER_SLOT(2) CAP_GATHER_SLOT(3)
+    CAP_GATHER_SLOT(4) CAP_GATHER_SLOT(5) CAP_GATHER_SLOT(6) CAP_GATHER_SLOT(7)
+#undef CAP_GATHER_SLOT
     float S = 0.0f;
 #pragma unroll
-    for (int s = 0; s < KI; ++s) {
-        w[s] = 0.0f;
-        if (s < k) {
-            w[s] = gate_exp(lv[s] - lv[0]);
-            S = S + w[s];
-        }
-    }
+    for (int s = 0; s < K; ++s) S = S + qs[s];
+    float ws[K];                               // every slot's gate, on every lane
 #pragma unroll
-    for (int s = 0; s < KI; ++s) w[s] = (s < k) ? w[s] / S : 0.0f;
+    for (int s = 0; s < K; ++s) ws[s] = qs[s] / S;
 
     // ---- device-level pruning
     const int src = (live ? t : 0) / tokens_per_rank;
     const int src_node = src / ranks_per_node;
-    int dev[KI];
-    int first[KI];
+    // lane g is a candidate if slot g is the first slot of its device;
+    // a = that device's score summed in slot order
+    bool cand = has_slot;
+    float a = 0.0f;
 #pragma unroll
-    for (int s = 0; s < KI; ++s) {
-        dev[s] = (s < k) ? er_lds[li[s] < E ? li[s] : 0] : -1;
-        first[s] = s;
+    for (int s = 0; s < K; ++s) {
+        const bool same = devs[s] == my_dev;
+        if (s < g) cand = cand && !same;
+        a = a + ((s >= g && same) ? ws[s] : 0.0f);
     }
-#pragma unroll
-    for (int s = 1; s < KI; ++s)
-#pragma unroll
-        for (int s2 = s - 1; s2 >= 0; --s2)
-            if (s < k && dev[s2] == dev[s]) first[s] = s2;
-
-    float a[KI];
-#pragma unroll
-    for (int j = 0; j < KI; ++j) a[j] = 0.0f;
-#pragma unroll
-    for (int s = 0; s < KI; ++s)
-#pragma unroll
-        for (int j = 0; j <= s; ++j)
-            if (s < k && first[s] == j) a[j] = a[j] + w[s];
-
-    bool cand[KI];
-    float key[KI];
-#pragma unroll
-    for (int j = 0; j < KI; ++j) {
-        cand[j] = (j < k) && first[j] == j;
-        const int d = dev[j];
-        if (d == src)
-            key[j] = INFINITY;
-        else if (d / ranks_per_node == src_node)
-            key[j] = a[j] / 1.0f;
-        else
-            key[j] = a[j] / inter_node_cost;
-    }
-    int rank[KI];
-#pragma unroll
-    for (int j = 0; j < KI; ++j) {
-        int r = 0;
-#pragma unroll
-        for (int j2 = 0; j2 < KI; ++j2)
-            if (cand[j2] && j2 != j &&
-                (key[j2] > key[j] || (key[j2] == key[j] && dev[j2] < dev[j])))
-                ++r;
-        rank[j] = r;
-    }
-    int stop_rank = KI;                  // keep every candidate unless the target is met earlier
-    if (p != 0.0f) {
-        const float target = 1.0f - p;
-        float cum = 0.0f;
-        bool done = false;
-#pragma unroll
-        for (int r = 0; r < KI; ++r) {
-#pragma unroll
-            for (int j = 0; j < KI; ++j) {
-                if (!done && cand[j] && rank[j] == r) {
-                    cum = cum + a[j];
-                    if (cum >= target) { stop_rank = r; done = true; }
-                }
-            }
-        }
-    }
+    float ratio = a;
+    if (my_dev == src) ratio = INFINITY;
+    else if (R > ranks_per_node && my_dev / ranks_per_node != src_node) ratio = a / inter_node_cost;
+    const uint64_t kbits = (1ull << 61) | (static_cast<uint64_t>(__float_as_uint(ratio)) << 30) |
+                           (static_cast<uint64_t>(63 - (my_dev & 63)) << 3);
+    double ck = cand ? __longlong_as_double(static_cast<long long>(kbits)) : kNoKey;
+    float ca = a;
+    // descending sort across the group (bitonic, mirrored first step per stage)
+    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+    lane_cx<kDppMirror4>(ck, ca, (g & 3) < 2);
+    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+    lane_cx<kDppHalfMirror>(ck, ca, g < 4);
+    lane_cx<kDppXor2>(ck, ca, (g & 2) == 0);
+    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+    // greedy retention in key order, replayed by every lane
+    const uint32_t ck_hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ck)) >> 32);
+    const int ck_lo = static_cast<int>(static_cast<uint64_t>(__double_as_longlong(ck)));
+    const float target = 1.0f - p;
+    const bool keep_all = (p == 0.0f);
+    float cum = 0.0f;
+    bool done = false;
     uint64_t mask = 0;
-    bool keep[KI];
-#pragma unroll
-    for (int j = 0; j < KI; ++j)
-        if (cand[j] && rank[j] <= stop_rank) mask |= 1ull << dev[j];
+#define CAP_GREEDY_STEP(S_)                                                          \
+    if constexpr (S_ < K) {                                                          \
+        const bool c2 = (group_lane<S_>(static_cast<int>(ck_hi)) >> 29) == 1;        \
+        const float a2 = group_lane<S_>(ca);                                         \
+        const int d2 = 63 - ((group_lane<S_>(ck_lo) >> 3) & 63);                     \
+        if (c2 && (keep_all || !done)) mask |= 1ull << d2;                           \
+        cum = cum + (c2 ? a2 : 0.0f);                                                \
+        done = done || (c2 && cum >= target);                                        \
+    }
+    CAP_GREEDY_STEP(0) CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
+    CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6) CAP_GREEDY_STEP(7)
+#undef CAP_GREEDY_STEP
     float Sk = 0.0f;
 #pragma unroll
-    for (int s = 0; s < KI; ++s) {
-        keep[s] = (s < k) && ((mask >> dev[s]) & 1ull);
-        if (keep[s]) Sk = Sk + w[s];
-    }
+    for (int s = 0; s < K; ++s) Sk = Sk + (((mask >> devs[s]) & 1ull) ? ws[s] : 0.0f);
 
     // ---- lane g writes slot g
-    if (live) {
-        int my_idx = 0;
-        float my_w = 0.0f;
-        uint8_t my_keep = 0;
+    if (live && has_slot) {
+        float my_w = ws[0];
 #pragma unroll
-        for (int s = 0; s < KI; ++s) {
-            if (s == g) {
-                my_idx = li[s];
-                my_w = keep[s] ? w[s] / Sk : 0.0f;
-                my_keep = keep[s] ? 1 : 0;
-            }
-        }
-        if (g < k) {
-            const size_t q = static_cast<size_t>(t) * k + g;
-            out_idx[q] = my_idx;
-            out_w[q] = my_w;
-            out_keep[q] = my_keep;
-        }
+        for (int s = 1; s < K; ++s) my_w = (g == s) ? ws[s] : my_w;
+        const bool my_keep = (mask >> my_dev) & 1ull;
+        const size_t qi = static_cast<size_t>(t) * K + g;
+        out_idx[qi] = my_e;
+        out_w[qi] = my_keep ? my_w / Sk : 0.0f;
+        out_keep[qi] = my_keep ? 1 : 0;
         if (g == 0) out_mask[t] = mask;
     }
 }
 
-template <int V, int KI>
+template <int V, int K>
 void launch_route(const cap_topology* tp, const float* logits, float p, int vec_ok,
                   int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
     const int blocks = (tp->T + kTokensPerBlock - 1) / kTokensPerBlock;
-    route_prune_kernel<V, KI><<<blocks, 256, 0, st>>>(
-        logits, tp->T, tp->E, tp->k, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
-        tp->inter_node_cost, p, vec_ok, tp->expert_rank, idx, w, keep, mask);
+    if (vec_ok)
+        route_prune_kernel<V, K, true><<<blocks, 256, 0, st>>>(
+            logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
+            tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
+    else
+        route_prune_kernel<V, K, false><<<blocks, 256, 0, st>>>(
+            logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
+            tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
 }
 
 template <int V>
 void launch_route_k(const cap_topology* tp, const float* logits, float p, int vec_ok,
                     int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
-    if (tp->k <= 1) launch_route<V, 1>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
-    else if (tp->k <= 2) launch_route<V, 2>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
-    else if (tp->k <= 4) launch_route<V, 4>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
-    else launch_route<V, 8>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
+    switch (tp->k) {
+        case 1: launch_route<V, 1>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 2: launch_route<V, 2>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 3: launch_route<V, 3>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 4: launch_route<V, 4>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 5: launch_route<V, 5>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 6: launch_route<V, 6>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 7: launch_route<V, 7>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        default: launch_route<V, 8>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+    }
 }
 
 }  // namespace
