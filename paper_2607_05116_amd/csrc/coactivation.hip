@@ -1,87 +1,159 @@
 // Expert co-activation counts on the pruned routing (Sec. IV-B: how often two
 // experts are selected together; Sec. VII: placement runs on pruned traces).
 //
+// C[i][j] counts, over tokens, the ordered pairs of kept slots (s, s') with
+// experts (i, j); s == s' gives the diagonal N_i.  C is symmetric, so only the
+// upper triangle i <= j is accumulated (row-major, E(E+1)/2 entries); a pair
+// of distinct slots adds 1 to (min, max), or 2 when both slots name the same
+// expert (both orders land on the diagonal).
+//
 // Two launches, no global atomics, deterministic (integer sums):
-//   1. tile    block (row group of 16 experts, token split): an LDS tile
-//              [16][E] of counts; each token adds 1 to (i, j) for every kept
-//              expert i in the row group and every kept expert j (i == j gives
-//              the diagonal N_i).  LDS integer atomics: the sum is order
-//              independent.  The tile is written to its split's partial slab.
-//   2. reduce  coact[i][j] = (accumulate ? coact[i][j] : 0) + sum over splits,
-//              in split order.
-// Workspace: [S][E][E] uint32 partials.
+//   1. tile    one block per split of consecutive tokens: the whole triangle
+//              in LDS as packed 16-bit counters (two per 32-bit word; a split
+//              holds at most 512 tokens and a token adds at most k^2 = 64 to
+//              one counter, so none reaches 2^16), LDS integer atomics (order
+//              independent), written to the split's partial slab.
+//   2. reduce  every packed word summed over the splits (split groups in
+//              parallel, then a fixed-order LDS sum), unpacked and written to
+//              (i, j) and (j, i), added to C when accumulating.
+// Workspace: [S][ceil(E(E+1)/4)] uint32 packed partials.
 #include "cap_device.hpp"
+
+#include <math.h>
 
 namespace cap {
 namespace {
 
-constexpr int kRows = 16;
 constexpr int kThreads = 256;
+constexpr int kMaxSplitTokens = 512;   // <= 512 tokens x k^2 pairs stays below 2^16
+constexpr int kMaxSplits = 2048;
+constexpr int kTriWordsMax = (kMaxE * (kMaxE + 1) / 2 + 1) / 2;
+constexpr int kReduceWords = 32;                       // words per reduce block
+constexpr int kReduceGroups = kThreads / kReduceWords; // split groups per reduce block
+
+__host__ __device__ inline int tri_size(int E) { return E * (E + 1) / 2; }
+__host__ __device__ inline int tri_words(int E) { return (tri_size(E) + 1) / 2; }
+__device__ __forceinline__ int row_start(int i, int E) { return i * E - i * (i - 1) / 2; }
+__device__ __forceinline__ int tri_index(int i, int j, int E) { return row_start(i, E) + (j - i); }
 
 __global__ __launch_bounds__(kThreads) void coact_tile_kernel(
     int T, int k, int E, int tokens_per_split, const int32_t* __restrict__ idx,
     const uint8_t* __restrict__ keep, uint32_t* __restrict__ part) {
-    __shared__ uint32_t tile[kRows * kMaxE];
-    const int r0 = blockIdx.x * kRows;
-    const int split = blockIdx.y;
-    for (int i = threadIdx.x; i < kRows * E; i += kThreads) tile[i] = 0;
+    __shared__ uint32_t tri[kTriWordsMax];
+    const int TW = tri_words(E);
+    for (int i = threadIdx.x; i < TW; i += kThreads) tri[i] = 0;
     __syncthreads();
-    const int t_begin = split * tokens_per_split;
+    const int t_begin = blockIdx.x * tokens_per_split;
     const int t_end = min(T, t_begin + tokens_per_split);
     for (int t = t_begin + threadIdx.x; t < t_end; t += kThreads) {
         int e[kMaxK];
-        int n = 0;
-        for (int s = 0; s < k; ++s) {
-            const size_t q = static_cast<size_t>(t) * k + s;
-            const int x = idx[q];
-            if (keep[q] && static_cast<unsigned>(x) < static_cast<unsigned>(E)) e[n++] = x;
+        bool kp[kMaxK];
+        const size_t q0 = static_cast<size_t>(t) * k;
+#pragma unroll
+        for (int s = 0; s < kMaxK; ++s) {
+            e[s] = 0;
+            kp[s] = false;
+            if (s < k) {
+                e[s] = idx[q0 + s];
+                kp[s] = keep[q0 + s] != 0;
+            }
         }
-        for (int a = 0; a < n; ++a) {
-            const int i = e[a] - r0;
-            if (static_cast<unsigned>(i) >= static_cast<unsigned>(kRows)) continue;
-            for (int b = 0; b < n; ++b) atomicAdd(&tile[i * E + e[b]], 1u);
+#pragma unroll
+        for (int s = 0; s < kMaxK; ++s) kp[s] = kp[s] && static_cast<unsigned>(e[s]) < static_cast<unsigned>(E);
+#pragma unroll
+        for (int a = 0; a < kMaxK; ++a) {
+#pragma unroll
+            for (int b = a; b < kMaxK; ++b) {
+                if (kp[a] && kp[b]) {
+                    const int i = min(e[a], e[b]), j = max(e[a], e[b]);
+                    const int x = tri_index(i, j, E);
+                    const uint32_t inc = (a != b && i == j) ? 2u : 1u;
+                    atomicAdd(&tri[x >> 1], inc << ((x & 1) * 16));
+                }
+            }
         }
     }
     __syncthreads();
-    const int rows = min(kRows, E - r0);
-    uint32_t* out = part + (static_cast<size_t>(split) * E + r0) * E;
-    for (int i = threadIdx.x; i < rows * E; i += kThreads) out[i] = tile[i];
+    uint32_t* out = part + static_cast<size_t>(blockIdx.x) * TW;
+    for (int i = threadIdx.x; i < TW; i += kThreads) out[i] = tri[i];
+}
+
+// (i, j) of triangle entry x (row-major upper triangle of an E x E matrix).
+__device__ __forceinline__ void tri_coords(int x, int E, int& i, int& j) {
+    const double b = 2.0 * E + 1.0;
+    int r = static_cast<int>((b - sqrt(b * b - 8.0 * x)) * 0.5);
+    r = max(0, min(E - 1, r));
+    if (r + 1 < E && row_start(r + 1, E) <= x) ++r;
+    if (r > 0 && row_start(r, E) > x) --r;
+    i = r;
+    j = r + (x - row_start(r, E));
 }
 
 __global__ __launch_bounds__(kThreads) void coact_reduce_kernel(
     int E, int splits, int accumulate, const uint32_t* __restrict__ part, uint32_t* __restrict__ coact) {
-    const int n = E * E;
-    for (int i = blockIdx.x * kThreads + threadIdx.x; i < n; i += gridDim.x * kThreads) {
-        uint32_t v = accumulate ? coact[i] : 0u;
-        for (int s = 0; s < splits; ++s) v += part[static_cast<size_t>(s) * n + i];
-        coact[i] = v;
+    __shared__ uint32_t lo_s[kReduceGroups][kReduceWords];
+    __shared__ uint32_t hi_s[kReduceGroups][kReduceWords];
+    const int TW = tri_words(E);
+    const int wl = threadIdx.x % kReduceWords;
+    const int grp = threadIdx.x / kReduceWords;
+    const int w = blockIdx.x * kReduceWords + wl;
+    uint32_t lo = 0, hi = 0;
+    if (w < TW) {
+        for (int s0 = grp * 8; s0 < splits; s0 += kReduceGroups * 8) {
+            uint32_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = (s0 + u < splits) ? part[static_cast<size_t>(s0 + u) * TW + w] : 0u;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                lo += v[u] & 0xFFFFu;
+                hi += v[u] >> 16;
+            }
+        }
+    }
+    lo_s[grp][wl] = lo;
+    hi_s[grp][wl] = hi;
+    __syncthreads();
+    if (grp < 2 && w < TW) {
+        uint32_t sum = 0;
+#pragma unroll
+        for (int g2 = 0; g2 < kReduceGroups; ++g2) sum += grp == 0 ? lo_s[g2][wl] : hi_s[g2][wl];
+        const int x = 2 * w + grp;
+        if (x < tri_size(E)) {
+            int i, j;
+            tri_coords(x, E, i, j);
+            const size_t ij = static_cast<size_t>(i) * E + j;
+            const size_t ji = static_cast<size_t>(j) * E + i;
+            coact[ij] = (accumulate ? coact[ij] : 0u) + sum;
+            if (i != j) coact[ji] = (accumulate ? coact[ji] : 0u) + sum;
+        }
     }
 }
 
-int coact_splits(int T, int E) {
-    const int row_groups = (E + kRows - 1) / kRows;
-    int s = (512 + row_groups - 1) / row_groups;     // aim for ~512 tile blocks
-    const int max_s = (T + 255) / 256;               // at least 256 tokens per split
-    if (s > max_s) s = max_s;
-    if (s > 64) s = 64;
-    return s < 1 ? 1 : s;
+int coact_tokens_per_split(int T) {
+    int per = 256;
+    while (per < kMaxSplitTokens && (T + per - 1) / per > kMaxSplits) per *= 2;
+    return per;
+}
+
+int coact_splits(int T) {
+    const int per = coact_tokens_per_split(T);
+    return (T + per - 1) / per;
 }
 
 }  // namespace
 
 size_t coact_workspace_bytes(int T, int E) {
-    return static_cast<size_t>(coact_splits(T, E)) * E * E * sizeof(uint32_t);
+    return static_cast<size_t>(coact_splits(T)) * tri_words(E) * sizeof(uint32_t);
 }
 
 cap_status coactivation_launch(int T, int k, int E, const int32_t* idx, const uint8_t* keep, uint32_t* coact,
                                int accumulate, void* ws, hipStream_t st) {
-    const int S = coact_splits(T, E);
-    const int per = (T + S - 1) / S;
-    dim3 grid((E + kRows - 1) / kRows, S);
+    const int per = coact_tokens_per_split(T);
+    const int S = coact_splits(T);
     uint32_t* part = static_cast<uint32_t*>(ws);
-    coact_tile_kernel<<<grid, kThreads, 0, st>>>(T, k, E, per, idx, keep, part);
+    coact_tile_kernel<<<S, kThreads, 0, st>>>(T, k, E, per, idx, keep, part);
     CAP_LAUNCH_CHECK();
-    const int blocks = (E * E + kThreads - 1) / kThreads;
+    const int blocks = (tri_words(E) + kReduceWords - 1) / kReduceWords;
     coact_reduce_kernel<<<blocks, kThreads, 0, st>>>(E, S, accumulate, part, coact);
     CAP_LAUNCH_CHECK();
     return CAP_OK;

@@ -101,6 +101,31 @@ def test_route_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
     assert np.array_equal(Ld.host("coact").view(np.uint32), oracle.coactivation(r["idx"], r["keep"], E))
 
 
+@pytest.mark.parametrize("T,k,E", [(600_000, 8, 256), (200_000, 8, 128), (1000, 3, 7), (1, 1, 1)])
+def test_coactivation_duplicates_and_many_splits(T, k, E):
+    """Random expert ids (duplicates within a token included) and random keep
+    flags, up to 600k tokens (the largest split size), straight through the
+    C-ABI, accumulating onto a nonzero start."""
+    rng = np.random.default_rng(T + E)
+    idx = rng.integers(0, E, (T, k), dtype=np.int32)
+    keep = (rng.random((T, k)) < 0.7).astype(np.uint8)
+    start = rng.integers(0, 1000, (E, E)).astype(np.uint32)
+    dev = torch.device("cuda:0")
+    idx_d = torch.from_numpy(idx).to(dev)
+    keep_d = torch.from_numpy(keep).to(dev)
+    coact_d = torch.from_numpy(start.view(np.int32)).to(dev)
+    ws_bytes = capi.cap_workspace_size(capi.CAP_OP_COACTIVATION, _coact_topo(T, E))
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
+    capi.cap_coactivation(T, k, E, idx_d, keep_d, coact_d, True, ws, ws_bytes)
+    torch.cuda.synchronize()
+    want = start + oracle.coactivation(idx, keep, E)
+    assert np.array_equal(coact_d.cpu().numpy().view(np.uint32), want)
+
+
+def _coact_topo(T, E):
+    return capi.Topology(E=E, R=1, ranks_per_node=1, T=T, tokens_per_rank=T, k=1)
+
+
 def test_determinism_front_end():
     case = C.ROUTE_CASES[5]
     L = _layer(case, row_cap=8, recv_cap=8)
