@@ -36,6 +36,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     return static_cast<uint32_t>(f32_to_bf16(a)) | (static_cast<uint32_t>(f32_to_bf16(b)) << 16);
 }
 
+// Two fp32 -> packed bf16x2 with the hardware conversion (v_cvt_pk_bf16_f32,
+// round to nearest even: the same bits as pack_bf16x2 for finite inputs).
+typedef __bf16 bf16x2_hw __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2_rne(float a, float b) {
+    const bf16x2_hw v = {static_cast<__bf16>(a), static_cast<__bf16>(b)};
+    return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 // Mask of lanes below the calling lane.

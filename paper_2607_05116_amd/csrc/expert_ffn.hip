@@ -82,15 +82,19 @@ __device__ __forceinline__ int worker_id() {
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
-// LDS ring of kStages stages; a stage holds the A tile [BM][32] and the B tile
-// [BN][32] (bf16, 64-byte rows).  16-byte chunk c of row r sits at physical
-// chunk c ^ lds_swz(r): fragment reads (rows r..r+15, one chunk) then hit
-// distinct banks for both 128- and 256-byte bank windows.
-constexpr int kStageK = 32;                 // K per stage
-constexpr int kStages = 4;                  // prefetch distance kStages - 1
+// LDS holds kStages stages; a stage is the A tile [BM][64] and the B tile
+// [BN][64] (bf16, 128-byte rows).  A stage row is one whole 128-byte line of
+// the K-contiguous operand: the direct-to-LDS path moves full lines at about
+// twice the rate of half lines, which is what sets the stage depth to K = 64.
+// 16-byte chunk c of row r sits at physical chunk c ^ lds_swz(r); fragment
+// reads (16 consecutive rows, one chunk) then hit distinct banks for both 128-
+// and 256-byte bank windows.
+constexpr int kStageK = 64;                 // K per stage
+constexpr int kStages = 2;                  // double buffer: prefetch distance 1
 constexpr int kRowB = kStageK * 2;          // bytes per LDS row
+constexpr int kChunks = kRowB / 16;         // 16-byte chunks per row
 
-__device__ __forceinline__ int lds_swz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+__device__ __forceinline__ int lds_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 
 // Workgroup barrier without the memory fence that __syncthreads() carries (the
 // fence would drain every in-flight prefetch).  LDS visibility is ensured by
@@ -103,13 +107,29 @@ __device__ __forceinline__ void block_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Wait until at most n of this wave's vector-memory operations are in flight.
-// Loads complete in issue order, so with n = (loads issued after the stage we
-// need) that stage has landed in LDS; pending stores only make it stricter.
+// Wait until at most n of this wave's vector-memory operations are in flight
+// (n rounded down to a multiple of 4, at most 60).  Vector-memory operations
+// complete in issue order, so with n = (operations issued after the stage we
+// need) that stage has landed in LDS; waiting for fewer is only stricter.
 __device__ __forceinline__ void wait_vmem(int n) {
-    if (n >= 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-    else if (n >= 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    switch (n >= 60 ? 15 : n >> 2) {
+        case 15: asm volatile("s_waitcnt vmcnt(60)" ::: "memory"); break;
+        case 14: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
+        case 13: asm volatile("s_waitcnt vmcnt(52)" ::: "memory"); break;
+        case 12: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+        case 11: asm volatile("s_waitcnt vmcnt(44)" ::: "memory"); break;
+        case 10: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+        case 9: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
+        case 8: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+        case 7: asm volatile("s_waitcnt vmcnt(28)" ::: "memory"); break;
+        case 6: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+        case 5: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
+        case 4: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+        case 3: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+        case 2: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+        case 1: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    }
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -146,15 +166,15 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     constexpr int NW = WAVES_M * WAVES_N;
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int MI = WM / 32, NJ = WN / 32;
+    constexpr int KS = kStageK / 16;                       // MFMA K steps per stage
     constexpr int ROWS_PER_LOAD = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
     constexpr int A_LD = BM / ROWS_PER_LOAD / NW;          // direct loads per wave per stage
     constexpr int B_LD = BN / ROWS_PER_LOAD / NW;
     constexpr int STAGE_B = (BM + BN) * kRowB;
-    constexpr int LOADS_PER_STAGE = A_LD + B_LD;
     static_assert(BM % (ROWS_PER_LOAD * NW) == 0 && BN % (ROWS_PER_LOAD * NW) == 0, "load split");
-    static_assert(LOADS_PER_STAGE == 8, "wait_vmem assumes 8 loads per stage");
     static_assert(!GATEUP || (WN % 64 == 0), "gate/up pairs need 64-column wave tiles");
-    static_assert(ROWS_PER_LOAD * NW >= 32 || !GATEUP, "a direct load must stay inside one W1/W3 block");
+    static_assert(32 % ROWS_PER_LOAD == 0, "a direct load must stay inside one W1/W3 block");
+    static_assert(KS % 2 == 0, "fragments are read two K steps at a time");
 
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE_B];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
@@ -165,54 +185,51 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     const int n_tiles = GATEUP ? N_out / (BN / 2) : N_out / BN;
     const int total = mt_prefix[E_loc] * n_tiles;
     const int KT = K / kStageK;
-    const int tid = threadIdx.x;
-    const int wave = tid / kWave, lane = tid % kWave;
-    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
-    const uint32_t wave_u = __builtin_amdgcn_readfirstlane(wave);
+    const int lane = threadIdx.x % kWave;
+    const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    const int wm = static_cast<int>(wave_u) / WAVES_N, wn = static_cast<int>(wave_u) % WAVES_N;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
 
-    // direct-load lane mapping: lane l writes LDS row (l >> 2), physical chunk
-    // (l & 3) of its 1 KiB block, so it fetches logical chunk (l & 3) ^ swz.
-    const int ld_row = lane >> 2;
-    const int ld_col = (((lane & 3) ^ lds_swz(ld_row)) * 8);        // elements
+    // direct-load lane mapping: lane l writes row (l >> 3) of its 1 KiB block
+    // at physical chunk (l & 7), so it fetches logical chunk (l & 7) ^ swz(row)
+    // (the swizzle of a tile row depends on the block parity too).
+    const int ld_row = lane >> 3;
+    const int ld_pc = lane & (kChunks - 1);
+    auto ld_col = [&](int blk) { return (ld_pc ^ lds_swz(blk * ROWS_PER_LOAD + ld_row)) * 8; };  // elements
     // fragment lane mapping (row r = ... + (lane & 31); swz depends on lane & 31 only)
     const int fr_row = lane & 31;
     const int fr_swz = lds_swz(fr_row);
     const int fr_half = lane >> 5;
 
-    // Per-tile load sources: wave-uniform byte bases (scalar) plus per-lane
-    // 32-bit byte offsets.  A rows past the expert's end are clamped to its
-    // last row (their results are never stored).
+    // Per-tile load sources: wave-uniform byte bases (scalar).  A rows past the
+    // expert's end are clamped to its last row (their results are never stored).
     struct TileSrc {
         const char* a;              // A + row0 * K
-        uint32_t a_off[A_LD];       // lane offsets within the tile rows
-        const char* b[B_LD];        // row block of each B load
+        int a_last;                 // last valid row of the tile
+        const char* b[B_LD];        // 8-row block of each B load
     };
-    const uint32_t b_lane_off = static_cast<uint32_t>(ld_row * K + ld_col) * 2u;
-    auto tile_sources = [&](int tile, int& l, int& row0, int& rows_valid, int& nt) {
+    auto tile_sources = [&](int tile, int& row0, int& rows_valid, int& nt) {
         TileSrc src;
         const int m_tile = tile / n_tiles;
         nt = tile % n_tiles;
-        l = find_expert(mt_prefix, E_loc, m_tile);
-        row0 = row_begin[l] + (m_tile - mt_prefix[l]) * BM;
-        rows_valid = min(BM, row_end[l] - row0);
+        // wave-uniform: keep them in scalar registers
+        const int l = __builtin_amdgcn_readfirstlane(find_expert(mt_prefix, E_loc, m_tile));
+        row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (m_tile - mt_prefix[l]) * BM);
+        rows_valid = __builtin_amdgcn_readfirstlane(min(BM, row_end[l] - row0));
         src.a = reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
-#pragma unroll
-        for (int i = 0; i < A_LD; ++i) {
-            const int r = (wave * A_LD + i) * ROWS_PER_LOAD + ld_row;
-            src.a_off[i] = static_cast<uint32_t>(min(r, rows_valid - 1) * K + ld_col) * 2u;
-        }
+        src.a_last = rows_valid - 1;
 #pragma unroll
         for (int i = 0; i < B_LD; ++i) {
-            const int blk = wave_u * B_LD + i;                 // 16-row block of the B tile
+            const int blk = wave_u * B_LD + i;                 // 8-row block of the B tile
             size_t row;
             const uint16_t* W = B0;
             if constexpr (GATEUP) {
-                const int q = blk >> 1;                        // W1 / W3 alternate per 32 rows
+                const int q = blk / (32 / ROWS_PER_LOAD);      // 32-row block: W1 / W3 alternate
                 W = (q & 1) ? B1 : B0;
-                row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + (q >> 1) * 32 + (blk & 1) * 16;
+                row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + (q >> 1) * 32 +
+                      (blk % (32 / ROWS_PER_LOAD)) * ROWS_PER_LOAD;
             } else {
-                row = static_cast<size_t>(l) * N_out + nt * BN + blk * 16;
+                row = static_cast<size_t>(l) * N_out + nt * BN + blk * ROWS_PER_LOAD;
             }
             src.b[i] = reinterpret_cast<const char*>(W + row * K);
         }
@@ -222,19 +239,29 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * STAGE_B);
         const size_t kb = static_cast<size_t>(kt) * kStageK * 2;
 #pragma unroll
-        for (int i = 0; i < A_LD; ++i) lds_dma16(src.a + kb, src.a_off[i], st + (wave_u * A_LD + i) * 1024);
+        for (int i = 0; i < A_LD; ++i) {
+            const int blk = static_cast<int>(wave_u) * A_LD + i;
+            const int r = min(blk * ROWS_PER_LOAD + ld_row, src.a_last);
+            lds_dma16(src.a + kb, static_cast<uint32_t>(r * K + ld_col(blk)) * 2u, st + blk * 1024);
+        }
 #pragma unroll
-        for (int i = 0; i < B_LD; ++i)
-            lds_dma16(src.b[i] + kb, b_lane_off, st + BM * kRowB + (wave_u * B_LD + i) * 1024);
+        for (int i = 0; i < B_LD; ++i) {
+            const int blk = static_cast<int>(wave_u) * B_LD + i;
+            lds_dma16(src.b[i] + kb, static_cast<uint32_t>(ld_row * K + ld_col(blk)) * 2u,
+                      st + BM * kRowB + blk * 1024);
+        }
     };
 
     int tile = worker_id();
-    int l = 0, row0 = 0, rows_valid = 0, nt = 0;
+    int row0 = 0, rows_valid = 0, nt = 0;
     TileSrc src;
     if (tile < total) {
-        src = tile_sources(tile, l, row0, rows_valid, nt);
-        for (int s = 0; s < kStages - 1 && s < KT; ++s) issue_stage(src, s);
+        src = tile_sources(tile, row0, rows_valid, nt);
+        issue_stage(src, 0);
     }
+    // The previous tile's epilogue stores were issued after this tile's stage
+    // 0, so the wait for stage 0 also counts them.
+    int pending_stores = 0;
     while (tile < total) {
         f32x16 acc[MI][NJ];
 #pragma unroll
@@ -245,83 +272,88 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
         for (int kt = 0; kt < KT; ++kt) {
-            wait_vmem(LOADS_PER_STAGE * min(kStages - 2, KT - 1 - kt));
-            block_barrier();                       // stage kt visible; stage kt-1 free
-            if (kt + kStages - 1 < KT) issue_stage(src, kt + kStages - 1);
+            wait_vmem(kt == 0 ? pending_stores : 0);
+            block_barrier();                       // stage kt visible; the other buffer is free
+            if (kt + 1 < KT) issue_stage(src, kt + 1);
             const uint8_t* sa = lds + (kt % kStages) * STAGE_B;
             const uint8_t* sb = sa + BM * kRowB;
-            bf16x8 fa[2][MI], fb[2][NJ];
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
+            for (int k2 = 0; k2 < KS; k2 += 2) {
+                bf16x8 fa[2][MI], fb[2][NJ];
 #pragma unroll
-                for (int i = 0; i < MI; ++i)
-                    fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * WM + i * 32 + fr_row) * kRowB + pc);
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int pc = ((2 * (k2 + ks) + fr_half) ^ fr_swz) << 4;
 #pragma unroll
-                for (int j = 0; j < NJ; ++j)
-                    fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * WN + j * 32 + fr_row) * kRowB + pc);
-            }
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-                for (int i = 0; i < MI; ++i)
+                    for (int i = 0; i < MI; ++i)
+                        fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * WM + i * 32 + fr_row) * kRowB + pc);
 #pragma unroll
                     for (int j = 0; j < NJ; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
-            // issue all fragment reads of the slice first, then the MFMAs
-            __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MI + NJ), 0);   // DS reads
-            __builtin_amdgcn_sched_group_barrier(0x008, 2 * MI * NJ, 0);     // MFMA
+                        fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * WN + j * 32 + fr_row) * kRowB + pc);
+                }
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+                    for (int i = 0; i < MI; ++i)
+#pragma unroll
+                        for (int j = 0; j < NJ; ++j)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+                __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MI + NJ), 0);   // DS reads
+                __builtin_amdgcn_sched_group_barrier(0x008, 2 * MI * NJ, 0);     // MFMA
+            }
         }
 
-        // every wave is done with this tile's LDS: start the next tile's loads,
-        // then write this tile's outputs while they are in flight
+        // every wave is done with this tile's LDS: start the next tile's first
+        // stage, then write this tile's outputs while it is in flight
         block_barrier();
-        const int cur_l = l, cur_row0 = row0, cur_rows = rows_valid, cur_nt = nt;
-        (void)cur_l;
+        const int cur_row0 = row0, cur_rows = rows_valid, cur_nt = nt;
         const int next = tile + gridDim.x;
         if (next < total) {
-            src = tile_sources(next, l, row0, rows_valid, nt);
-            for (int s = 0; s < kStages - 1 && s < KT; ++s) issue_stage(src, s);
+            src = tile_sources(next, row0, rows_valid, nt);
+            issue_stage(src, 0);
         }
 
-        // epilogue: lane holds token row m = lane % 32 of each 32-row block and,
-        // per register group g, output columns 8g + 4*(lane/32) + 0..3 of each
-        // 32-column block.
-        const int n_sub = fr_half * 4;
+        // Epilogue.  Lane (r, h) = (lane % 32, lane / 32) holds, for register
+        // group g, columns 8g + 4h + 0..3 of row r of each 32x32 block.  Lanes
+        // r and r + 32 swap halves (permlane32_swap) so that each writes 8
+        // consecutive columns: groups (0, 1) -> lane r columns 0..7, lane r + 32
+        // columns 8..15; groups (2, 3) likewise at 16 and 24.  Two 16-byte
+        // stores per lane per block; blocks with no valid row are skipped by
+        // the whole wave, so every issued store is counted in pending_stores.
+        pending_stores = 0;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
+            if (wm * WM + i * 32 >= cur_rows) continue;                 // wave-uniform
             const int mr = wm * WM + i * 32 + fr_row;
-            if (mr >= cur_rows) continue;
+            const bool row_ok = mr < cur_rows;
             uint16_t* crow = C + static_cast<size_t>(cur_row0 + mr) * N_out;
-            if constexpr (GATEUP) {
+            constexpr int NB = GATEUP ? NJ / 2 : NJ;                    // output blocks per i
 #pragma unroll
-                for (int jp = 0; jp < NJ / 2; ++jp) {
-                    const int j0 = cur_nt * (BN / 2) + (wn * WN / 64 + jp) * 32;
+            for (int jb = 0; jb < NB; ++jb) {
+                float v[16];
+                int c0;
+                if constexpr (GATEUP) {
+                    c0 = cur_nt * (BN / 2) + (wn * WN / 64 + jb) * 32;
 #pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        float h[4];
+                    for (int e = 0; e < 16; ++e) v[e] = silu(acc[i][2 * jb][e]) * acc[i][2 * jb + 1][e];
+                } else {
+                    c0 = cur_nt * BN + wn * WN + jb * 32;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e)
-                            h[e] = silu(acc[i][2 * jp][4 * g + e]) * acc[i][2 * jp + 1][4 * g + e];
-                        uint2 v;
-                        v.x = pack_bf16x2(h[0], h[1]);
-                        v.y = pack_bf16x2(h[2], h[3]);
-                        *reinterpret_cast<uint2*>(crow + j0 + 8 * g + n_sub) = v;
-                    }
+                    for (int e = 0; e < 16; ++e) v[e] = acc[i][jb][e];
                 }
-            } else {
 #pragma unroll
-                for (int j = 0; j < NJ; ++j) {
-                    const int c0 = cur_nt * BN + wn * WN + j * 32;
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        uint2 v;
-                        v.x = pack_bf16x2(acc[i][j][4 * g + 0], acc[i][j][4 * g + 1]);
-                        v.y = pack_bf16x2(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-                        *reinterpret_cast<uint2*>(crow + c0 + 8 * g + n_sub) = v;
-                    }
+                for (int gp = 0; gp < 4; gp += 2) {
+                    const uint32_t x0 = pack_bf16x2_rne(v[4 * gp + 0], v[4 * gp + 1]);
+                    const uint32_t x1 = pack_bf16x2_rne(v[4 * gp + 2], v[4 * gp + 3]);
+                    const uint32_t y0 = pack_bf16x2_rne(v[4 * gp + 4], v[4 * gp + 5]);
+                    const uint32_t y1 = pack_bf16x2_rne(v[4 * gp + 6], v[4 * gp + 7]);
+                    const auto ra = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+                    const auto rb = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+                    u32x4 out;
+                    out[0] = ra[0]; out[1] = rb[0]; out[2] = ra[1]; out[3] = rb[1];
+                    if (row_ok) *reinterpret_cast<u32x4*>(crow + c0 + 8 * (gp + fr_half)) = out;
                 }
             }
+            pending_stores += 2 * NB;
         }
         tile = next;
     }
@@ -400,7 +432,11 @@ __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(
 }
 
 // Tile configurations (bf16).
-constexpr int kBM = 256, kBN = 256, kWavesM = 2, kWavesN = 2;
+#ifndef CAP_FFN_WAVES_M
+#define CAP_FFN_WAVES_M 4
+#define CAP_FFN_WAVES_N 2
+#endif
+constexpr int kBM = 256, kBN = 256, kWavesM = CAP_FFN_WAVES_M, kWavesN = CAP_FFN_WAVES_N;
 
 int persistent_grid(long long tiles_upper) {
     const long long cus = device_cu_count();
