@@ -7,16 +7,18 @@
 //   down      Y[m][o] = (H W2^T)[m][o]                         (K = inter)
 //
 // bf16 path (gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation):
-//   * Block tile BM x BN (K sliced by 32), waves arranged WAVES_M x WAVES_N, each wave a
-//     (BM/WAVES_M) x (BN/WAVES_N) sub-tile of 32x32 MFMA blocks.
+//   * Block tile 256 x 256, eight waves (two per SIMD) of 64 x 128 each.
 //   * Operands are both K-contiguous (token rows of X / H; weight rows of W).
-//     gfx950 direct-to-LDS loads (global_load_lds_dwordx4) fill a 4-stage LDS
-//     ring of 32-wide K slices, three stages ahead of the MFMAs, with no
-//     staging registers; one barrier per K slice.  The next tile's first
-//     stages are issued before the current tile's epilogue stores.
+//     gfx950 direct-to-LDS loads (global_load_lds_dwordx4) fill a double
+//     buffer of K = 64 stages: every operand row of a stage is one whole
+//     128-byte line, which the direct-to-LDS path moves at about twice the
+//     rate of half lines.  One barrier per stage.
+//   * Half of the waves issue all the stage loads and the other half all the
+//     output stores, so no wave's in-order memory counter mixes the two (a
+//     wait for a stage never waits for a tile's worth of stores to drain).
 //   * The MFMA is issued with the weight fragment as its first operand, so a
 //     lane's 16 accumulators hold 4 consecutive output columns per register
-//     group and the epilogue stores 8 bytes at a time.
+//     group; lanes r and r + 32 exchange halves so each stores 16 bytes.
 //   * Gate/up: the B tile interleaves 32-row blocks of W1 and W3 (W1 rows j..j+31,
 //     then W3 rows j..j+31, ...), so the gate and up accumulators of one output
 //     element sit in the same lane and register; SiLU-and-multiply happens in
@@ -27,10 +29,21 @@
 // fp32 path: a plain LDS-tiled FMA kernel (small shapes only).
 #include "cap_device.hpp"
 
+#include <type_traits>
+
 namespace cap {
 namespace {
 
 constexpr int kMaxExpertsLocal = kMaxE;
+
+// Compile-time loop: f(std::integral_constant<int, 0>) ... f(<N - 1>).
+template <int N, int I = 0, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
+    }
+}
 
 // ------------------------------------------------------------------ tile scheduler
 struct Sched {
@@ -80,6 +93,56 @@ __device__ __forceinline__ int worker_id() {
 // silu(g) = g * sigmoid(g); hardware exp2 and reciprocal (about 1 ulp each),
 // far inside the bf16 rounding that H then takes.
 __device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
+
+// Scalar base of a direct load: uniform by construction; readfirstlane keeps it
+// in scalar registers (widening through uint32_t so the low word is never
+// sign-extended).
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+    const uint64_t b = reinterpret_cast<uint64_t>(p);
+    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+    return reinterpret_cast<const void*>((hi << 32) | lo);
+}
+
+// Wave-wide copies global -> LDS (gfx950 global_load_lds_dwordx4): lane i
+// reads 16 bytes at base + voff_i and they land at LDS byte M0 + 16 * i; base
+// is a scalar register pair, voff a 32-bit per-lane byte offset, and the
+// instruction's immediate offset stays 0 (it would shift the LDS address too).
+// They are inline assembly so that the compiler's wait-count pass does not
+// treat every later LDS read as aliasing them (it would drain all in-flight
+// stages); the kernel waits on them explicitly with wait_vmem().  Because the
+// compiler does not see the instruction, it also does not insert the wait
+// states the hardware needs before it: a VALU write of an SGPR (v_readfirstlane
+// of the base) needs 5 wait states before a vector-memory instruction reads it,
+// and an SALU write of M0 needs 1 before an LDS DMA; the s_nop 4 inside each
+// statement provides 5.
+//
+// Direct load of row block I: byte offset lane_off + I * blk_bytes, formed
+// inside the statement (v_mad_u32_u24; both factors stay below 2^24) so the
+// compiler keeps no per-block offset registers alive across the K loop.
+template <int I>
+__device__ __forceinline__ void lds_dma16_blk(const void* base, uint32_t lane_off, uint32_t blk_bytes,
+                                              uint32_t lds_addr) {
+    uint32_t off;
+    asm volatile("v_mad_u32_u24 %0, %1, %2, %3\n\ts_nop 4\n\tglobal_load_lds_dwordx4 %0, %4"
+                 : "=&v"(off)
+                 : "n"(I), "s"(blk_bytes), "v"(lane_off), "s"(uniform_ptr(base)),
+                   "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
+
+// Direct load of rows first + ld_row, clamped to last (rows past an expert's
+// end repeat its last row): offset min(first + ld_row, last) * pitch + col_b.
+__device__ __forceinline__ void lds_dma16_clamped(const void* base, uint32_t ld_row, int first, int last,
+                                                  uint32_t pitch, uint32_t col_b, uint32_t lds_addr) {
+    uint32_t off;
+    asm volatile("v_add_u32 %0, %1, %2\n\tv_min_i32 %0, %3, %0\n\tv_mad_u32_u24 %0, %0, %4, %5\n\t"
+                 "s_nop 4\n\tglobal_load_lds_dwordx4 %0, %6"
+                 : "=&v"(off)
+                 : "s"(first), "v"(ld_row), "s"(last), "s"(pitch), "v"(col_b), "s"(uniform_ptr(base)),
+                   "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
 
 // ------------------------------------------------------------------ bf16 MFMA GEMM
 // LDS holds kStages stages; a stage is the A tile [BM][64] and the B tile
@@ -134,47 +197,43 @@ __device__ __forceinline__ void wait_vmem(int n) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// One wave-wide copy global -> LDS (gfx950 global_load_lds_dwordx4): lane i
-// reads 16 bytes at base + voff_i and they land at LDS byte lds_addr + 16 * i.
-// `base` is wave-uniform (scalar registers), voff a 32-bit per-lane byte
-// offset.  Issued as inline assembly so the compiler's wait-count pass does not
-// treat every later LDS read as aliasing it (it would drain all in-flight
-// stages); the kernel waits on these loads explicitly with wait_vmem().  The
-// instruction's immediate offset stays 0 (it would shift the LDS address too).
-// Because the compiler does not see the instruction, it also does not insert
-// the wait states the hardware needs before it: a VALU write of an SGPR
-// (v_readfirstlane of the base) needs 5 wait states before a vector-memory
-// instruction reads that SGPR, and an SALU write of M0 needs 1 before an LDS
-// DMA.  The s_nop 4 inside the statement provides 5.
-__device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
-    // The base is uniform by construction; say so, so it lives in scalar
-    // registers.  readfirstlane returns a signed int: widen through uint32_t so
-    // the low word is zero-extended, never sign-extended.
-    const uint64_t b = reinterpret_cast<uint64_t>(base);
-    const uint64_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
-    const uint64_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
-    const void* sbase = reinterpret_cast<const void*>((hi << 32) | lo);
-    asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff), "s"(sbase),
-                 "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr)) : "memory");
-}
 
+// Roles.  Loads and stores share one in-order completion counter per wave,
+// so a wave that stores its outputs and then waits for a stage would also
+// wait for every store to drain (a whole tile of outputs per CU, all CUs at
+// once).  The first half of the waves ("loaders") therefore issue every
+// direct-to-LDS stage load and never store to global memory: they leave their
+// outputs in an LDS staging area.  The other half ("storers") issue no loads;
+// they write their own outputs and the staged ones, and never wait for
+// stores.  The staging area is stage buffer 1, free from the end of a tile's K
+// loop until the next tile fills its stage 1 (one barrier later).
 template <int BM, int BN, int WAVES_M, int WAVES_N, bool GATEUP>
 __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
     uint16_t* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K,
     int N_out) {
     constexpr int NW = WAVES_M * WAVES_N;
+    constexpr int NL = NW / 2;                             // loader waves
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
     constexpr int MI = WM / 32, NJ = WN / 32;
     constexpr int KS = kStageK / 16;                       // MFMA K steps per stage
     constexpr int ROWS_PER_LOAD = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
-    constexpr int A_LD = BM / ROWS_PER_LOAD / NW;          // direct loads per wave per stage
-    constexpr int B_LD = BN / ROWS_PER_LOAD / NW;
+    constexpr int A_LD = BM / ROWS_PER_LOAD / NL;          // direct loads per loader wave per stage
+    constexpr int B_LD = BN / ROWS_PER_LOAD / NL;
     constexpr int STAGE_B = (BM + BN) * kRowB;
-    static_assert(BM % (ROWS_PER_LOAD * NW) == 0 && BN % (ROWS_PER_LOAD * NW) == 0, "load split");
+    constexpr int OUT_C = GATEUP ? WN / 2 : WN;            // output columns of a wave tile
+    constexpr int OUT_RB = OUT_C * 2;                      // bytes per staged output row
+    constexpr int OUT_CH = OUT_RB / 16;                    // 16-byte chunks per staged row
+    constexpr int OUT_RPW = 256 / OUT_RB;                  // staged rows per 256-byte bank window
+    constexpr int STG_B = WM * OUT_RB;                     // staging bytes per loader wave
+    static_assert(NW % 2 == 0 && NL % 4 == 0, "one loader and one storer wave per SIMD");
+    static_assert(BM % (ROWS_PER_LOAD * NL) == 0 && BN % (ROWS_PER_LOAD * NL) == 0, "load split");
+    static_assert(A_LD + B_LD <= 60, "loads per stage must fit the vmcnt field");
     static_assert(!GATEUP || (WN % 64 == 0), "gate/up pairs need 64-column wave tiles");
     static_assert(32 % ROWS_PER_LOAD == 0, "a direct load must stay inside one W1/W3 block");
     static_assert(KS % 2 == 0, "fragments are read two K steps at a time");
+    static_assert(kStages == 2 && NL * STG_B <= STAGE_B, "staging lives in stage buffer 1");
+    static_assert(OUT_RB == 128 || OUT_RB == 256, "staged row layout");
 
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE_B];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
@@ -187,26 +246,35 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     const int KT = K / kStageK;
     const int lane = threadIdx.x % kWave;
     const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int wm = static_cast<int>(wave_u) / WAVES_N, wn = static_cast<int>(wave_u) % WAVES_N;
+    const int wave = static_cast<int>(wave_u);
+    const bool loader = wave < NL;
+    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
+    uint8_t* const staging = lds + STAGE_B;                // stage buffer 1
 
     // direct-load lane mapping: lane l writes row (l >> 3) of its 1 KiB block
     // at physical chunk (l & 7), so it fetches logical chunk (l & 7) ^ swz(row)
     // (the swizzle of a tile row depends on the block parity too).
     const int ld_row = lane >> 3;
     const int ld_pc = lane & (kChunks - 1);
-    auto ld_col = [&](int blk) { return (ld_pc ^ lds_swz(blk * ROWS_PER_LOAD + ld_row)) * 8; };  // elements
     // fragment lane mapping (row r = ... + (lane & 31); swz depends on lane & 31 only)
     const int fr_row = lane & 31;
     const int fr_swz = lds_swz(fr_row);
     const int fr_half = lane >> 5;
+    // staged output rows: 16-byte chunk c of row r at physical chunk
+    // c ^ ((r / OUT_RPW) % OUT_CH), conflict-free for column writes and row reads
+    auto stg_swz = [&](int r) { return (r / OUT_RPW) & (OUT_CH - 1); };
 
-    // Per-tile load sources: wave-uniform byte bases (scalar).  A rows past the
-    // expert's end are clamped to its last row (their results are never stored).
+    // Per-tile load sources (loader waves): wave-uniform byte bases.  A rows
+    // past the expert's end are clamped to its last row (never stored).
+    // A loader's B rows are one contiguous run (down) or two (gate/up: its
+    // W1 rows, then the matching W3 rows), so two scalar bases cover them.
+    constexpr int B_RUN = GATEUP ? B_LD / 2 : B_LD;        // loads per contiguous B run
+    static_assert(!GATEUP || B_RUN * ROWS_PER_LOAD == 32, "a gate/up loader covers one 32-row W1/W3 pair");
     struct TileSrc {
         const char* a;              // A + row0 * K
         int a_last;                 // last valid row of the tile
-        const char* b[B_LD];        // 8-row block of each B load
+        const char* b[2];           // first row of each B run
     };
     auto tile_sources = [&](int tile, int& row0, int& rows_valid, int& nt) {
         TileSrc src;
@@ -218,38 +286,49 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         rows_valid = __builtin_amdgcn_readfirstlane(min(BM, row_end[l] - row0));
         src.a = reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
         src.a_last = rows_valid - 1;
-#pragma unroll
-        for (int i = 0; i < B_LD; ++i) {
-            const int blk = wave_u * B_LD + i;                 // 8-row block of the B tile
-            size_t row;
-            const uint16_t* W = B0;
-            if constexpr (GATEUP) {
-                const int q = blk / (32 / ROWS_PER_LOAD);      // 32-row block: W1 / W3 alternate
-                W = (q & 1) ? B1 : B0;
-                row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + (q >> 1) * 32 +
-                      (blk % (32 / ROWS_PER_LOAD)) * ROWS_PER_LOAD;
-            } else {
-                row = static_cast<size_t>(l) * N_out + nt * BN + blk * ROWS_PER_LOAD;
-            }
-            src.b[i] = reinterpret_cast<const char*>(W + row * K);
+        const int lw = loader ? wave : 0;
+        if constexpr (GATEUP) {
+            const size_t row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + lw * 32;
+            src.b[0] = reinterpret_cast<const char*>(B0 + row * K);
+            src.b[1] = reinterpret_cast<const char*>(B1 + row * K);
+        } else {
+            const size_t row = static_cast<size_t>(l) * N_out + nt * BN + lw * B_LD * ROWS_PER_LOAD;
+            src.b[0] = src.b[1] = reinterpret_cast<const char*>(B0 + row * K);
         }
         return src;
     };
+    // Lane byte offsets of a direct load within its 8-row block: the swizzle
+    // of row (blk * 8 + ld_row) is ld_row ^ (blk & 1), so two values cover
+    // every block; the block's own row offset is added inside the load.
+    const uint32_t col_b[2] = {static_cast<uint32_t>((ld_pc ^ lds_swz(ld_row)) * 16),
+                               static_cast<uint32_t>((ld_pc ^ lds_swz(ROWS_PER_LOAD + ld_row)) * 16)};
+    const uint32_t pitch = static_cast<uint32_t>(K) * 2u;                 // bytes per operand row
+    const uint32_t lane_off[2] = {ld_row * pitch + col_b[0], ld_row * pitch + col_b[1]};
+    const uint32_t blk_bytes = static_cast<uint32_t>(ROWS_PER_LOAD) * pitch;
     auto issue_stage = [&](const TileSrc& src, int kt) {
+        if (!loader) return;
         const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * STAGE_B);
         const size_t kb = static_cast<size_t>(kt) * kStageK * 2;
-#pragma unroll
-        for (int i = 0; i < A_LD; ++i) {
-            const int blk = static_cast<int>(wave_u) * A_LD + i;
-            const int r = min(blk * ROWS_PER_LOAD + ld_row, src.a_last);
-            lds_dma16(src.a + kb, static_cast<uint32_t>(r * K + ld_col(blk)) * 2u, st + blk * 1024);
+        const char* a_base = src.a + kb + static_cast<size_t>(wave * A_LD) * blk_bytes;
+        const uint32_t a_lds = st + wave * A_LD * 1024;
+        const int a_first = wave * A_LD * ROWS_PER_LOAD;
+        if (a_first + A_LD * ROWS_PER_LOAD - 1 <= src.a_last) {                  // wave-uniform
+            static_for<A_LD>([&](auto I) {
+                lds_dma16_blk<I.value>(a_base, lane_off[(wave * A_LD + I.value) & 1], blk_bytes, a_lds + I.value * 1024);
+            });
+        } else {
+            // the last tile of an expert: rows past its end repeat its last row
+            static_for<A_LD>([&](auto I) {
+                lds_dma16_clamped(src.a + kb, ld_row, a_first + I.value * ROWS_PER_LOAD, src.a_last, pitch,
+                                  col_b[(wave * A_LD + I.value) & 1], a_lds + I.value * 1024);
+            });
         }
-#pragma unroll
-        for (int i = 0; i < B_LD; ++i) {
-            const int blk = static_cast<int>(wave_u) * B_LD + i;
-            lds_dma16(src.b[i] + kb, static_cast<uint32_t>(ld_row * K + ld_col(blk)) * 2u,
-                      st + BM * kRowB + blk * 1024);
-        }
+        const uint32_t b_lds = st + BM * kRowB + wave * B_LD * 1024;
+        static_for<B_LD>([&](auto I) {
+            constexpr int i = decltype(I)::value;
+            lds_dma16_blk<i % B_RUN>(src.b[i / B_RUN] + kb, lane_off[(wave * B_LD + i) & 1], blk_bytes,
+                                     b_lds + i * 1024);
+        });
     };
 
     int tile = worker_id();
@@ -259,9 +338,6 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         src = tile_sources(tile, row0, rows_valid, nt);
         issue_stage(src, 0);
     }
-    // The previous tile's epilogue stores were issued after this tile's stage
-    // 0, so the wait for stage 0 also counts them.
-    int pending_stores = 0;
     while (tile < total) {
         f32x16 acc[MI][NJ];
 #pragma unroll
@@ -272,7 +348,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
         for (int kt = 0; kt < KT; ++kt) {
-            wait_vmem(kt == 0 ? pending_stores : 0);
+            if (loader) wait_vmem(0);              // this wave's part of stage kt has landed
             block_barrier();                       // stage kt visible; the other buffer is free
             if (kt + 1 < KT) issue_stage(src, kt + 1);
             const uint8_t* sa = lds + (kt % kStages) * STAGE_B;
@@ -302,8 +378,8 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
             }
         }
 
-        // every wave is done with this tile's LDS: start the next tile's first
-        // stage, then write this tile's outputs while it is in flight
+        // every wave is done with this tile's LDS: loaders start the next
+        // tile's stage 0 (buffer 0), buffer 1 becomes the staging area
         block_barrier();
         const int cur_row0 = row0, cur_rows = rows_valid, cur_nt = nt;
         const int next = tile + gridDim.x;
@@ -314,29 +390,26 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
 
         // Epilogue.  Lane (r, h) = (lane % 32, lane / 32) holds, for register
         // group g, columns 8g + 4h + 0..3 of row r of each 32x32 block.  Lanes
-        // r and r + 32 swap halves (permlane32_swap) so that each writes 8
+        // r and r + 32 swap halves (permlane32_swap) so that each holds 8
         // consecutive columns: groups (0, 1) -> lane r columns 0..7, lane r + 32
-        // columns 8..15; groups (2, 3) likewise at 16 and 24.  Two 16-byte
-        // stores per lane per block; blocks with no valid row are skipped by
-        // the whole wave, so every issued store is counted in pending_stores.
-        pending_stores = 0;
+        // columns 8..15; groups (2, 3) likewise at 16 and 24.  Loaders write
+        // those 16 bytes to staging, storers to the output.
+        uint8_t* my_stg = staging + (loader ? wave : 0) * STG_B;
+        const int out_c0 = GATEUP ? cur_nt * (BN / 2) + wn * (WN / 2) : cur_nt * BN + wn * WN;
 #pragma unroll
         for (int i = 0; i < MI; ++i) {
-            if (wm * WM + i * 32 >= cur_rows) continue;                 // wave-uniform
-            const int mr = wm * WM + i * 32 + fr_row;
-            const bool row_ok = mr < cur_rows;
-            uint16_t* crow = C + static_cast<size_t>(cur_row0 + mr) * N_out;
-            constexpr int NB = GATEUP ? NJ / 2 : NJ;                    // output blocks per i
+            if (!loader && wm * WM + i * 32 >= cur_rows) continue;      // wave-uniform
+            const int r = i * 32 + fr_row;                              // row within the wave tile
+            const bool row_ok = wm * WM + r < cur_rows;
+            uint16_t* crow = C + static_cast<size_t>(cur_row0 + wm * WM + r) * N_out + out_c0;
+            constexpr int NB = GATEUP ? NJ / 2 : NJ;                    // 32-column output blocks
 #pragma unroll
             for (int jb = 0; jb < NB; ++jb) {
                 float v[16];
-                int c0;
                 if constexpr (GATEUP) {
-                    c0 = cur_nt * (BN / 2) + (wn * WN / 64 + jb) * 32;
 #pragma unroll
                     for (int e = 0; e < 16; ++e) v[e] = silu(acc[i][2 * jb][e]) * acc[i][2 * jb + 1][e];
                 } else {
-                    c0 = cur_nt * BN + wn * WN + jb * 32;
 #pragma unroll
                     for (int e = 0; e < 16; ++e) v[e] = acc[i][jb][e];
                 }
@@ -350,10 +423,32 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
                     const auto rb = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
                     u32x4 out;
                     out[0] = ra[0]; out[1] = rb[0]; out[2] = ra[1]; out[3] = rb[1];
-                    if (row_ok) *reinterpret_cast<u32x4*>(crow + c0 + 8 * (gp + fr_half)) = out;
+                    const int c = jb * 4 + gp + fr_half;                // 8-column chunk in the wave tile
+                    if (loader) {
+                        *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = out;
+                    } else if (row_ok) {
+                        *reinterpret_cast<u32x4*>(crow + 8 * c) = out;
+                    }
                 }
             }
-            pending_stores += 2 * NB;
+        }
+        block_barrier();                                                // staging written
+        if (!loader) {
+            // storer wave w writes the staged tile of loader wave w - NL
+            const int lw = wave - NL;
+            const int lwm = lw / WAVES_N, lwn = lw % WAVES_N;
+            const uint8_t* stg = staging + lw * STG_B;
+            const int l_c0 = GATEUP ? cur_nt * (BN / 2) + lwn * (WN / 2) : cur_nt * BN + lwn * WN;
+            constexpr int ROWS_PER_READ = 1024 / OUT_RB;
+#pragma unroll
+            for (int r0 = 0; r0 < WM; r0 += ROWS_PER_READ) {
+                if (lwm * WM + r0 >= cur_rows) break;                   // wave-uniform
+                const int r = r0 + lane / OUT_CH;
+                const int c = lane % OUT_CH;
+                const u32x4 vv = *reinterpret_cast<const u32x4*>(stg + r * OUT_RB + 16 * (c ^ stg_swz(r)));
+                if (lwm * WM + r < cur_rows)
+                    *reinterpret_cast<u32x4*>(C + static_cast<size_t>(cur_row0 + lwm * WM + r) * N_out + l_c0 + 8 * c) = vv;
+            }
         }
         tile = next;
     }
@@ -432,11 +527,7 @@ __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(
 }
 
 // Tile configurations (bf16).
-#ifndef CAP_FFN_WAVES_M
-#define CAP_FFN_WAVES_M 4
-#define CAP_FFN_WAVES_N 2
-#endif
-constexpr int kBM = 256, kBN = 256, kWavesM = CAP_FFN_WAVES_M, kWavesN = CAP_FFN_WAVES_N;
+constexpr int kBM = 256, kBN = 256, kWavesM = 4, kWavesN = 2;
 
 int persistent_grid(long long tiles_upper) {
     const long long cus = device_cu_count();
