@@ -213,7 +213,8 @@ def test_ffn_f32_ragged_experts():
     assert C.rel_fro(got, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("name,kind,p", [("c2", "coact", 0.3), ("c2", "seq", 0.0), ("c4", "coact", 0.1)])
+@pytest.mark.parametrize("name,kind,p", [("c2", "coact", 0.3), ("c2", "seq", 0.0), ("c4", "coact", 0.1),
+                                         ("c3", "coact", 0.1), ("c5", "coact", 0.1)])
 def test_ffn_full_size_sampled_rows(name, kind, p):
     """Rank 0's expert FFN at the workload's real shape; sampled rows vs the oracle."""
     case = C.Case(name, gen.CONFIGS[name], kind, p)
@@ -241,6 +242,44 @@ def test_ffn_full_size_sampled_rows(name, kind, p):
         if len(sel):
             W1, W3, W2 = gen.expert_weights_f32(cfg, ids[l])
             ref[sel] = oracle.swiglu_rows(xs_all[sample[sel]], W1, W3, W2)
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+
+
+@pytest.mark.parametrize("name", ["c4", "c5"])
+def test_shared_experts_and_src_reduce(name):
+    """Shared experts at the workload's real shape: the shared SwiGLU (one FFN
+    over the concatenated intermediate size) on sampled rank-0 tokens against
+    the oracle, then the source reduce with the shared output added."""
+    cfg = gen.CONFIGS[name]
+    kind, p = "coact", 0.1
+    case = C.Case(name, cfg, kind, p)
+    er, el = C.placement(name, kind, p, 5.0)
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = _layer(case, x=x)
+    L.set_shared_weights(*gen.shared_weights(cfg))
+    L.front()
+    L.shared_ffn(0)
+    torch.cuda.synchronize()
+    T_loc = cfg.tokens_per_rank
+    rng = np.random.default_rng(4)
+    sample = np.sort(rng.choice(T_loc, size=48, replace=False))
+    got = L.shared_out[torch.from_numpy(sample).cuda()].float().cpu().numpy()
+    W1, W3, W2 = gen.shared_weights_f32(cfg)
+    ref = oracle.swiglu_rows(gen.bf16_bits_to_f32(x[sample]), W1, W3, W2)
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+    n_recv = int(lay["recv_offsets"][-1])
+    parts = gen.random_rows(n_recv, cfg.d, "bf16", salt=5)
+    L.parts[:n_recv] = torch.from_numpy(parts.view(np.int16)).view(torch.bfloat16).cuda()
+    L.src_reduce(0)
+    torch.cuda.synchronize()
+    shared = L.shared_out.float().cpu().numpy()
+    ref = oracle.src_reduce(gen.bf16_bits_to_f32(parts), r, lay, er, cfg.R, T_loc, 0, cfg.d, shared=shared)
+    got = L.y.float().cpu().numpy()
     ok, worst = C.within_tol(got, ref)
     assert ok, worst
     assert C.rel_fro(got, ref) <= 1e-2
