@@ -296,6 +296,24 @@ def main():
     }
     hbm = {s: round(kbytes[s] / (stage_ms[s] * 1e-3) / 1e9, 1) for s in kbytes if stage_ms[s] > 0}
 
+    # CAP's device-level pruning against expert-level threshold pruning at the
+    # same p (untimed): kept slots, destinations and send volume per token
+    def volume(tot, kept):
+        return {"kept_slot_frac": kept / (cfg.T * cfg.k), "device_per_token": int(tot[0]) / cfg.T,
+                "node_per_token": int(tot[3]) / cfg.T,
+                "send_bytes_per_token": int(tot[1] + tot[2]) * cfg.d * eb / cfg.T,
+                "send_bytes_per_token_inter": int(tot[2]) * cfg.d * eb / cfg.T}
+    pruning = {"p": args.p, "cap": volume(totals, int(L.host("keep").sum()))}
+    L.naive = True
+    L.route()
+    L.layout()
+    torch.cuda.synchronize()
+    pruning["naive"] = volume(L.host("totals").astype(np.int64), int(L.host("keep").sum()))
+    L.naive = False
+    L.route()
+    L.layout()
+    torch.cuda.synchronize()
+
     result = {
         "metric": METRIC,
         "value": cfg.tokens_per_rank / (ms_per_step * 1e-3),
@@ -334,6 +352,7 @@ def main():
             "device_per_token": int(totals[0]) / cfg.T,
             "node_per_token": int(totals[3]) / cfg.T,
             "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
+            "pruning_cap_vs_naive": pruning,
             "rank_rows": rows, "rank_received_tokens": U,
             "host_wall_ms_per_step": 1e3 * wall / K,
         },

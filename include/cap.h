@@ -181,6 +181,19 @@ cap_status cap_route_prune(const cap_topology *topo, const float *logits, float 
                            void *stream);
 
 /*
+ * Expert-level threshold pruning: the baseline CAP is compared with (Sec. II-D;
+ * the naive strategy of Sec. VIII-D).  Same arguments, top-k and gates as
+ * cap_route_prune; the pruning keeps the shortest prefix of slots (descending
+ * score) whose fp32 running sum of w_s reaches 1 - p (p == 0 keeps every
+ * slot), renormalises the kept gates the same way, and sets dst_mask to the
+ * devices of the kept slots.  It ignores where experts are placed, so it
+ * removes fewer devices than cap_route_prune at the same p.  No workspace.
+ */
+cap_status cap_route_prune_naive(const cap_topology *topo, const float *logits, float p,
+                                 int32_t *idx, float *w, uint8_t *keep, uint64_t *dst_mask,
+                                 void *stream);
+
+/*
  * Counting and prefix scans into the all-to-all send layout, the expert-sorted
  * layout and per-token send volume (Sec. II-C device-centric transfer; Eq. 3
  * topology classes).  Inputs: the outputs of cap_route_prune.  Outputs: every

@@ -5,7 +5,7 @@ every computation runs in the HIP kernels of libcap.so.  There is no CPU
 fallback: importing this module raises if the library is missing, and every
 call raises CapError on a non-zero status.
 
-Function names follow the C ABI: cap_route_prune, cap_dispatch_layout,
+Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_dispatch_layout,
 cap_permute, cap_expert_ffn, cap_combine, cap_coactivation,
 cap_workspace_size, cap_status_string, cap_version.
 """
@@ -26,7 +26,7 @@ CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 (CAP_OP_ROUTE_PRUNE, CAP_OP_DISPATCH_LAYOUT, CAP_OP_PERMUTE, CAP_OP_EXPERT_FFN,
  CAP_OP_COMBINE, CAP_OP_COACTIVATION) = range(6)
 
-EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune",
+EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_combine",
            "cap_coactivation"]
 
@@ -62,6 +62,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "cap_version": ([], i32),
         "cap_workspace_size": ([ctypes.c_int, P(Topology), i32, i32, i32, ctypes.c_int], sz),
         "cap_route_prune": ([P(Topology), vp, f32, vp, vp, vp, vp, vp], ctypes.c_int),
+        "cap_route_prune_naive": ([P(Topology), vp, f32, vp, vp, vp, vp, vp], ctypes.c_int),
         "cap_dispatch_layout": ([P(Topology), vp, vp, vp, P(Layout), vp, sz, vp], ctypes.c_int),
         "cap_permute": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, vp, vp, vp, P(Layout),
                          vp, i32, vp], ctypes.c_int),
@@ -124,6 +125,12 @@ def cap_workspace_size(op: int, topo: Topology | None, d: int = 0, inter: int = 
                        dtype: int = CAP_DTYPE_BF16) -> int:
     return _lib.cap_workspace_size(op, ctypes.byref(topo) if topo is not None else None,
                                    d, inter, max_rows, dtype)
+
+
+def cap_route_prune_naive(topo, logits, p, idx, w, keep, dst_mask, stream=None):
+    _check("cap_route_prune_naive", _lib.cap_route_prune_naive(
+        ctypes.byref(topo), _ptr(logits), float(p), _ptr(idx), _ptr(w), _ptr(keep), _ptr(dst_mask),
+        _stream(stream)))
 
 
 def cap_route_prune(topo, logits, p, idx, w, keep, dst_mask, stream=None):

@@ -7,7 +7,7 @@
 
 namespace cap {
 
-cap_status route_prune_launch(const cap_topology*, const float*, float, int32_t*, float*, uint8_t*, uint64_t*,
+cap_status route_prune_launch(const cap_topology*, const float*, float, bool, int32_t*, float*, uint8_t*, uint64_t*,
                               hipStream_t);
 size_t layout_workspace_bytes(const cap_topology*);
 cap_status dispatch_layout_launch(const cap_topology*, const int32_t*, const uint8_t*, const uint64_t*,
@@ -108,7 +108,14 @@ cap_status cap_route_prune(const cap_topology* topo, const float* logits, float 
                            uint8_t* keep, uint64_t* dst_mask, void* stream) {
     if (!topo_ok(topo) || !logits || !idx || !w || !keep || !dst_mask) return CAP_ERR_INVALID_ARG;
     if (!(p >= 0.0f) || !(p < 1.0f)) return CAP_ERR_INVALID_ARG;
-    return route_prune_launch(topo, logits, p, idx, w, keep, dst_mask, as_stream(stream));
+    return route_prune_launch(topo, logits, p, false, idx, w, keep, dst_mask, as_stream(stream));
+}
+
+cap_status cap_route_prune_naive(const cap_topology* topo, const float* logits, float p, int32_t* idx, float* w,
+                                 uint8_t* keep, uint64_t* dst_mask, void* stream) {
+    if (!topo_ok(topo) || !logits || !idx || !w || !keep || !dst_mask) return CAP_ERR_INVALID_ARG;
+    if (!(p >= 0.0f) || !(p < 1.0f)) return CAP_ERR_INVALID_ARG;
+    return route_prune_launch(topo, logits, p, true, idx, w, keep, dst_mask, as_stream(stream));
 }
 
 cap_status cap_dispatch_layout(const cap_topology* topo, const int32_t* idx, const uint8_t* keep,

@@ -174,7 +174,7 @@ __device__ __forceinline__ void lane_cx(double& key, float& a, bool lower) {
 }
 constexpr int kDppMirror4 = 0x1B;       // quad_perm [3,2,1,0]
 
-template <int V, int K, bool VEC>
+template <int V, int K, bool VEC, bool NAIVE>
 __global__ __launch_bounds__(256) void route_prune_kernel(
     const float* __restrict__ logits, int T, int E, int R, int ranks_per_node,
     int tokens_per_rank, float inter_node_cost, float p,
@@ -273,63 +273,79 @@ __global__ __launch_bounds__(256) void route_prune_kernel(
 #pragma unroll
     for (int s = 0; s < K; ++s) ws[s] = qs[s] / S;
 
-    // ---- device-level pruning
-    const int src = (live ? t : 0) / tokens_per_rank;
-    const int src_node = src / ranks_per_node;
-    // lane g is a candidate if slot g is the first slot of its device;
-    // a = that device's score summed in slot order
-    bool cand = has_slot;
-    float a = 0.0f;
-#pragma unroll
-    for (int s = 0; s < K; ++s) {
-        const bool same = devs[s] == my_dev;
-        if (s < g) cand = cand && !same;
-        a = a + ((s >= g && same) ? ws[s] : 0.0f);
-    }
-    float ratio = a;
-    if (my_dev == src) ratio = INFINITY;
-    else if (R > ranks_per_node && my_dev / ranks_per_node != src_node) ratio = a / inter_node_cost;
-    const uint64_t kbits = (1ull << 61) | (static_cast<uint64_t>(__float_as_uint(ratio)) << 30) |
-                           (static_cast<uint64_t>(63 - (my_dev & 63)) << 3);
-    double ck = cand ? __longlong_as_double(static_cast<long long>(kbits)) : kNoKey;
-    float ca = a;
-    // descending sort across the group (bitonic, mirrored first step per stage)
-    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
-    lane_cx<kDppMirror4>(ck, ca, (g & 3) < 2);
-    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
-    lane_cx<kDppHalfMirror>(ck, ca, g < 4);
-    lane_cx<kDppXor2>(ck, ca, (g & 2) == 0);
-    lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
-    // greedy retention in key order, replayed by every lane
-    const uint32_t ck_hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ck)) >> 32);
-    const int ck_lo = static_cast<int>(static_cast<uint64_t>(__double_as_longlong(ck)));
+    // ---- pruning
     const float target = 1.0f - p;
     const bool keep_all = (p == 0.0f);
-    float cum = 0.0f;
-    bool done = false;
     uint64_t mask = 0;
-#define CAP_GREEDY_STEP(S_)                                                          \
-    if constexpr (S_ < K) {                                                          \
-        const bool c2 = (group_lane<S_>(static_cast<int>(ck_hi)) >> 29) == 1;        \
-        const float a2 = group_lane<S_>(ca);                                         \
-        const int d2 = 63 - ((group_lane<S_>(ck_lo) >> 3) & 63);                     \
-        if (c2 && (keep_all || !done)) mask |= 1ull << d2;                           \
-        cum = cum + (c2 ? a2 : 0.0f);                                                \
-        done = done || (c2 && cum >= target);                                        \
-    }
-    CAP_GREEDY_STEP(0) CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
-    CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6) CAP_GREEDY_STEP(7)
-#undef CAP_GREEDY_STEP
     float Sk = 0.0f;
+    int n_keep = K;                         // naive: slots kept (a prefix)
+    if constexpr (NAIVE) {
+        // expert level: the shortest slot prefix whose running score reaches 1 - p
+        float cum = 0.0f;
 #pragma unroll
-    for (int s = 0; s < K; ++s) Sk = Sk + (((mask >> devs[s]) & 1ull) ? ws[s] : 0.0f);
+        for (int s = 0; s < K; ++s) {
+            cum = cum + ws[s];
+            if (!keep_all && n_keep == K && cum >= target) n_keep = s + 1;
+        }
+#pragma unroll
+        for (int s = 0; s < K; ++s) {
+            if (s < n_keep) mask |= 1ull << devs[s];
+            Sk = Sk + ((s < n_keep) ? ws[s] : 0.0f);
+        }
+    } else {
+        const int src = (live ? t : 0) / tokens_per_rank;
+        const int src_node = src / ranks_per_node;
+        // lane g is a candidate if slot g is the first slot of its device;
+        // a = that device's score summed in slot order
+        bool cand = has_slot;
+        float a = 0.0f;
+#pragma unroll
+        for (int s = 0; s < K; ++s) {
+            const bool same = devs[s] == my_dev;
+            if (s < g) cand = cand && !same;
+            a = a + ((s >= g && same) ? ws[s] : 0.0f);
+        }
+        float ratio = a;
+        if (my_dev == src) ratio = INFINITY;
+        else if (R > ranks_per_node && my_dev / ranks_per_node != src_node) ratio = a / inter_node_cost;
+        const uint64_t kbits = (1ull << 61) | (static_cast<uint64_t>(__float_as_uint(ratio)) << 30) |
+                               (static_cast<uint64_t>(63 - (my_dev & 63)) << 3);
+        double ck = cand ? __longlong_as_double(static_cast<long long>(kbits)) : kNoKey;
+        float ca = a;
+        // descending sort across the group (bitonic, mirrored first step per stage)
+        lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+        lane_cx<kDppMirror4>(ck, ca, (g & 3) < 2);
+        lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+        lane_cx<kDppHalfMirror>(ck, ca, g < 4);
+        lane_cx<kDppXor2>(ck, ca, (g & 2) == 0);
+        lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
+        // greedy retention in key order, replayed by every lane
+        const uint32_t ck_hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ck)) >> 32);
+        const int ck_lo = static_cast<int>(static_cast<uint64_t>(__double_as_longlong(ck)));
+        float cum = 0.0f;
+        bool done = false;
+#define CAP_GREEDY_STEP(S_)                                                          \
+        if constexpr (S_ < K) {                                                          \
+            const bool c2 = (group_lane<S_>(static_cast<int>(ck_hi)) >> 29) == 1;        \
+            const float a2 = group_lane<S_>(ca);                                         \
+            const int d2 = 63 - ((group_lane<S_>(ck_lo) >> 3) & 63);                     \
+            if (c2 && (keep_all || !done)) mask |= 1ull << d2;                           \
+            cum = cum + (c2 ? a2 : 0.0f);                                                \
+            done = done || (c2 && cum >= target);                                        \
+        }
+        CAP_GREEDY_STEP(0) CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
+        CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6) CAP_GREEDY_STEP(7)
+#undef CAP_GREEDY_STEP
+#pragma unroll
+        for (int s = 0; s < K; ++s) Sk = Sk + (((mask >> devs[s]) & 1ull) ? ws[s] : 0.0f);
+    }
 
     // ---- lane g writes slot g
     if (live && has_slot) {
         float my_w = ws[0];
 #pragma unroll
         for (int s = 1; s < K; ++s) my_w = (g == s) ? ws[s] : my_w;
-        const bool my_keep = (mask >> my_dev) & 1ull;
+        const bool my_keep = NAIVE ? (g < n_keep) : ((mask >> my_dev) & 1ull);
         const size_t qi = static_cast<size_t>(t) * K + g;
         out_idx[qi] = my_e;
         out_w[qi] = my_keep ? my_w / Sk : 0.0f;
@@ -338,38 +354,45 @@ __global__ __launch_bounds__(256) void route_prune_kernel(
     }
 }
 
-template <int V, int K>
-void launch_route(const cap_topology* tp, const float* logits, float p, int vec_ok,
-                  int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
+template <int V, int K, bool NAIVE>
+void launch_route_mode(const cap_topology* tp, const float* logits, float p, int vec_ok,
+                       int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
     const int blocks = (tp->T + kTokensPerBlock - 1) / kTokensPerBlock;
     if (vec_ok)
-        route_prune_kernel<V, K, true><<<blocks, 256, 0, st>>>(
+        route_prune_kernel<V, K, true, NAIVE><<<blocks, 256, 0, st>>>(
             logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
             tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
     else
-        route_prune_kernel<V, K, false><<<blocks, 256, 0, st>>>(
+        route_prune_kernel<V, K, false, NAIVE><<<blocks, 256, 0, st>>>(
             logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
             tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
 }
 
+template <int V, int K>
+void launch_route(const cap_topology* tp, const float* logits, float p, bool naive, int vec_ok,
+                  int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
+    if (naive) launch_route_mode<V, K, true>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
+    else launch_route_mode<V, K, false>(tp, logits, p, vec_ok, idx, w, keep, mask, st);
+}
+
 template <int V>
-void launch_route_k(const cap_topology* tp, const float* logits, float p, int vec_ok,
+void launch_route_k(const cap_topology* tp, const float* logits, float p, bool naive, int vec_ok,
                     int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
     switch (tp->k) {
-        case 1: launch_route<V, 1>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 2: launch_route<V, 2>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 3: launch_route<V, 3>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 4: launch_route<V, 4>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 5: launch_route<V, 5>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 6: launch_route<V, 6>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 7: launch_route<V, 7>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        default: launch_route<V, 8>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 1: launch_route<V, 1>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 2: launch_route<V, 2>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 3: launch_route<V, 3>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 4: launch_route<V, 4>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 5: launch_route<V, 5>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 6: launch_route<V, 6>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 7: launch_route<V, 7>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        default: launch_route<V, 8>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
     }
 }
 
 }  // namespace
 
-cap_status route_prune_launch(const cap_topology* tp, const float* logits, float p, int32_t* idx,
+cap_status route_prune_launch(const cap_topology* tp, const float* logits, float p, bool naive, int32_t* idx,
                               float* w, uint8_t* keep, uint64_t* mask, hipStream_t st) {
     int V = 1;
     while (kGroup * V < tp->E) V <<= 1;
@@ -378,12 +401,12 @@ cap_status route_prune_launch(const cap_topology* tp, const float* logits, float
     // (every other E takes the bounds-checked scalar path).
     const int vec_ok = (tp->E == kGroup * V) && (reinterpret_cast<uintptr_t>(logits) % (4 * CW) == 0);
     switch (V) {
-        case 1: launch_route_k<1>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 2: launch_route_k<2>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 4: launch_route_k<4>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 8: launch_route_k<8>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        case 16: launch_route_k<16>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
-        default: launch_route_k<32>(tp, logits, p, vec_ok, idx, w, keep, mask, st); break;
+        case 1: launch_route_k<1>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 2: launch_route_k<2>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 4: launch_route_k<4>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 8: launch_route_k<8>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        case 16: launch_route_k<16>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
+        default: launch_route_k<32>(tp, logits, p, naive, vec_ok, idx, w, keep, mask, st); break;
     }
     CAP_LAUNCH_CHECK();
     return CAP_OK;

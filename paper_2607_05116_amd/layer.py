@@ -80,6 +80,7 @@ class DeviceLayer:
         self.ws_ffn = self._ws(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, cfg.inter,
                                                        self.row_cap, self.dt))
         self.weights: dict[int, tuple] = {}
+        self.naive = False              # expert-level threshold pruning instead of CAP's
         self.shared = None
         self.shared_out = None
         self.ws_shared = None
@@ -104,7 +105,8 @@ class DeviceLayer:
 
     # ------------------------------------------------------------ steps
     def route(self, stream=None):
-        capi.cap_route_prune(self.topo, self.logits, self.p, self.idx, self.w, self.keep, self.mask, stream)
+        fn = capi.cap_route_prune_naive if self.naive else capi.cap_route_prune
+        fn(self.topo, self.logits, self.p, self.idx, self.w, self.keep, self.mask, stream)
 
     def layout(self, stream=None):
         capi.cap_dispatch_layout(self.topo, self.idx, self.keep, self.mask, self.lay, self.ws_layout,

@@ -55,6 +55,30 @@ def test_route_layout_coact_bit_exact(case):
     assert np.array_equal(L.host("coact").view(np.uint32), coact)
 
 
+@pytest.mark.parametrize("case", C.ROUTE_CASES, ids=lambda c: c.id)
+def test_naive_pruning_bit_exact(case):
+    """Expert-level threshold pruning (the comparison baseline) against the
+    oracle: routing outputs and the layout built from them."""
+    L = _layer(case, row_cap=8, recv_cap=8)
+    L.naive = True
+    L.route()
+    L.layout()
+    torch.cuda.synchronize()
+    cfg = case.cfg
+    er, el = C.placement(case.name, case.placement, case.p, case.c)
+    logits = C.logits(case.name)
+    idx = oracle.topk(logits, cfg.k)
+    w = oracle.gates(logits, idx)
+    keep, wp, mask = oracle.prune_naive(idx, w, er, case.p)
+    assert np.array_equal(L.host("idx"), idx)
+    assert np.array_equal(L.host("w").view(np.uint32), wp.view(np.uint32))
+    assert np.array_equal(L.host("keep"), keep)
+    assert np.array_equal(L.host("mask").view(np.uint64), mask)
+    lay = oracle.dispatch_layout(idx, keep, mask, er, el, cfg.R, cfg.ranks_per_node, cfg.tokens_per_rank, cfg.E)
+    for name in ("send_counts", "expert_offsets", "slot_pos", "copy_row", "vol", "totals"):
+        assert np.array_equal(L.host(name), lay[name]), name
+
+
 def test_coactivation_accumulate():
     case = C.ROUTE_CASES[3]
     L = _layer(case, row_cap=8, recv_cap=8)

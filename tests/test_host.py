@@ -47,26 +47,33 @@ def _topo(capi, **over):
     return t
 
 
+ROUTE_FNS = ["cap_route_prune", "cap_route_prune_naive"]
+
+
+@pytest.mark.parametrize("fn", ROUTE_FNS)
 @pytest.mark.parametrize("over", [dict(k=0), dict(k=9), dict(E=300), dict(E=18), dict(R=65, E=130, T=260),
                                   dict(T=255), dict(ranks_per_node=3)])
-def test_route_prune_rejects_bad_topology(capi, over):
+def test_route_prune_rejects_bad_topology(capi, fn, over):
     t = _topo(capi, **over)
-    st = capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None)
+    st = getattr(capi._lib, fn)(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None)
     assert st == capi.CAP_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("fn", ROUTE_FNS)
 @pytest.mark.parametrize("p", [-0.1, 1.0, 1.5, float("nan")])
-def test_route_prune_rejects_bad_threshold(capi, p):
+def test_route_prune_rejects_bad_threshold(capi, fn, p):
     t = _topo(capi)
-    st = capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, p, 0x4000, 0x5000, 0x6000, 0x7000, None)
+    st = getattr(capi._lib, fn)(ctypes.byref(t), 0x3000, p, 0x4000, 0x5000, 0x6000, 0x7000, None)
     assert st == capi.CAP_ERR_INVALID_ARG
 
 
-def test_route_prune_rejects_null_and_bad_cost(capi):
+@pytest.mark.parametrize("fn", ROUTE_FNS)
+def test_route_prune_rejects_null_and_bad_cost(capi, fn):
     t = _topo(capi)
-    assert capi._lib.cap_route_prune(ctypes.byref(t), None, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
+    f = getattr(capi._lib, fn)
+    assert f(ctypes.byref(t), None, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
     t.inter_node_cost = 0.5
-    assert capi._lib.cap_route_prune(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
+    assert f(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
 
 
 def test_workspace_checks(capi):
