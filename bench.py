@@ -93,8 +93,45 @@ def product_placement(cfg, p, c):
     Lt.route()
     Lt.coactivation()
     C = Lt.host("coact").view(np.uint32)
-    return placement.coactivation_placement(C, cfg.R, cfg.ranks_per_node, gen.random_order(cfg.E, 0, 0),
-                                            gen.random_order(cfg.R, 0, 1))
+    er, el = placement.coactivation_placement(C, cfg.R, cfg.ranks_per_node, gen.random_order(cfg.E, 0, 0),
+                                              gen.random_order(cfg.R, 0, 1))
+    return er, el, C
+
+
+def placement_spectrum(L, cfg, C, er, el, c):
+    """CAP offline step 3 (Sec. V): the Adjustment Approach's placement
+    spectrum from the co-activation placement, 7 points evaluated on this
+    workload's pruned routing (devices per token, load imbalance of kept rows,
+    send volume) next to the sequential placement.  Untimed; restores the
+    placement afterwards."""
+    import numpy as np
+    import torch
+    from paper_2607_05116_amd import placement
+    from workloads import generator as gen
+    spec = placement.adjustment_spectrum(C, er, el, cfg.R, cfg.ranks_per_node, c)
+    P = placement.coactivation_probability(C)
+    def evaluate(ranks, local):
+        L.set_placement(ranks, local)
+        L.route()
+        L.layout()
+        torch.cuda.synchronize()
+        tot = L.host("totals").astype(np.int64)
+        rows = np.diff(L.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
+        return {"comm_objective": float(placement.comm_objective(P, np.asarray(ranks), cfg.ranks_per_node, c)),
+                "device_per_token": int(tot[0]) / cfg.T,
+                "load_imbalance": float(rows.max() / rows.mean()),
+                "send_bytes_per_token": int(tot[1] + tot[2]) * cfg.d * cfg.elem_bytes / cfg.T}
+    points = []
+    for i in placement.spectrum_points(len(spec)):
+        pt = evaluate(spec[i][0], spec[i][1])
+        pt["swaps"] = i
+        points.append(pt)
+    seq = evaluate(*gen.sequential_placement(cfg))
+    L.set_placement(er, el)
+    L.route()
+    L.layout()
+    torch.cuda.synchronize()
+    return {"total_swaps": len(spec) - 1, "points": points, "sequential": seq}
 
 
 def file_hash(path):
@@ -217,7 +254,7 @@ def main():
     logits = gen.logits(cfg)
     x = gen.activations(cfg)
     if args.placement == "coact":
-        er, el = product_placement(cfg, args.p, args.c)
+        er, el, coact_counts = product_placement(cfg, args.p, args.c)
     else:
         er, el = gen.sequential_placement(cfg)
     L = DeviceLayer(cfg, logits, x, er, el, args.p, args.c)
@@ -313,6 +350,11 @@ def main():
     L.route()
     L.layout()
     torch.cuda.synchronize()
+    spectrum = None
+    if args.placement == "coact":
+        t_spec = time.perf_counter()
+        spectrum = placement_spectrum(L, cfg, coact_counts, er, el, args.c)
+        log(f"placement spectrum: {spectrum['total_swaps']} swaps, {time.perf_counter() - t_spec:.1f} s")
 
     result = {
         "metric": METRIC,
@@ -353,6 +395,7 @@ def main():
             "node_per_token": int(totals[3]) / cfg.T,
             "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
             "pruning_cap_vs_naive": pruning,
+            "placement_spectrum": spectrum,
             "rank_rows": rows, "rank_received_tokens": U,
             "host_wall_ms_per_step": 1e3 * wall / K,
         },

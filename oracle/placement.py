@@ -121,3 +121,80 @@ def load_imbalance(loads):
     """Eq. 4: max_g L_g / mean_g L_g."""
     mean = sum(loads) / len(loads)
     return max(loads) / mean if mean > 0 else 0.0
+
+
+# ---------------------------------------------------------------- Adjustment Approach
+# Comm.-comp. trade-off adjustment (Sec. V): starting from the communication-
+# oriented placement, repeatedly swap a pair of experts between a high-load and
+# a low-load device, reducing load imbalance while losing as little
+# co-activation locality as possible; the successive placements form the
+# placement spectrum.  The paper leaves the pair choice open; the reading here:
+# * loads: L_g = sum of N_e over the experts on g, N_e = C[e][e] (kept
+#   (token, expert) pairs, the rows device g computes);
+# * each step swaps between the most loaded device (ties: lower id) and the
+#   least loaded one (ties: lower id);
+# * candidates: e on the most loaded device, f on the least loaded one, whose
+#   swap lowers the larger of the two loads (N_e > N_f and
+#   L_lo + N_e - N_f < L_hi);
+# * the chosen pair has the smallest increase of the communication objective
+#   (Eq. 2-3, recomputed from its definition; ties: lower e, then lower f);
+#   e and f exchange devices and local slots;
+# * the spectrum ends when no candidate remains (or after max_swaps).
+
+def expert_loads(C):
+    return [int(C[e][e]) for e in range(len(C))]
+
+
+def device_loads(N, expert_rank, R):
+    L = [0] * R
+    for e, g in enumerate(expert_rank):
+        L[g] += N[e]
+    return L
+
+
+def adjust_step(P, N, expert_rank, expert_local, R, ranks_per_node, c):
+    """One swap -> (expert_rank, expert_local, (e, f), delta_C), or None."""
+    L = device_loads(N, expert_rank, R)
+    hi = max(range(R), key=lambda g: (L[g], -g))
+    lo = min(range(R), key=lambda g: (L[g], g))
+    if L[hi] == L[lo]:
+        return None
+    base = comm_objective(P, expert_rank, ranks_per_node, c)
+    best = None
+    for e in range(len(N)):
+        if expert_rank[e] != hi:
+            continue
+        for f in range(len(N)):
+            if expert_rank[f] != lo:
+                continue
+            if not (N[e] > N[f] and L[lo] + N[e] - N[f] < L[hi]):
+                continue
+            trial = list(expert_rank)
+            trial[e], trial[f] = lo, hi
+            delta = comm_objective(P, trial, ranks_per_node, c) - base
+            if best is None or delta < best[2]:
+                best = (e, f, delta)
+    if best is None:
+        return None
+    e, f, delta = best
+    er = list(expert_rank)
+    el = list(expert_local)
+    er[e], er[f] = lo, hi
+    el[e], el[f] = expert_local[f], expert_local[e]
+    return er, el, (e, f), delta
+
+
+def adjustment_spectrum(C, expert_rank, expert_local, R, ranks_per_node, c, max_swaps=1 << 30):
+    """[(expert_rank, expert_local, swapped pair or None)] from the starting
+    placement through every swap until none applies."""
+    P = coactivation_probability(C)
+    N = expert_loads(C)
+    out = [(list(expert_rank), list(expert_local), None)]
+    er, el = list(expert_rank), list(expert_local)
+    for _ in range(max_swaps):
+        step = adjust_step(P, N, er, el, R, ranks_per_node, c)
+        if step is None:
+            break
+        er, el, pair, _ = step
+        out.append((er, el, pair))
+    return out

@@ -94,6 +94,12 @@ class DeviceLayer:
         """w1, w3 [E_loc][inter][d], w2 [E_loc][d][inter] in local-slot order (storage type)."""
         self.weights[rank] = tuple(to_device_rows(w, self.cfg.dtype, self.dev) for w in (w1, w3, w2))
 
+    def set_placement(self, expert_rank, expert_local):
+        """Replace the placement in place (the topology keeps pointing at the
+        same device arrays)."""
+        self.expert_rank.copy_(torch.as_tensor(np.asarray(expert_rank, np.int32)))
+        self.expert_local.copy_(torch.as_tensor(np.asarray(expert_local, np.int32)))
+
     def set_shared_weights(self, w1, w3, w2):
         self.shared = tuple(to_device_rows(w, self.cfg.dtype, self.dev) for w in (w1, w3, w2))
         inter = self.shared[0].shape[0]

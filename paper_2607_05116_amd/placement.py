@@ -105,3 +105,71 @@ def load_imbalance(loads) -> float:
     loads = np.asarray(loads, dtype=np.float64)
     m = loads.mean()
     return float(loads.max() / m) if m > 0 else 0.0
+
+
+# ---------------------------------------------------------------- Adjustment Approach (Sec. V)
+# Placement spectrum by load-balancing swaps, starting from the communication-
+# oriented placement.  Readings of what the paper leaves open (one line each):
+#   loads      L_g = sum of N_e over g's experts, N_e = C[e][e] (kept rows);
+#   devices    each step swaps between the most loaded device and the least
+#              loaded one (ties: lower id);
+#   candidates e on the former, f on the latter, whose swap lowers the larger
+#              of the two loads (N_e > N_f, L_lo + N_e - N_f < L_hi);
+#   choice     smallest increase of the Eq. 2-3 objective, each candidate's
+#              objective summed sequentially over i < j in row-major order
+#              (ties: lower e, then lower f); e and f exchange local slots;
+#   end        no candidate remains (or max_swaps).
+
+def _sequential_objectives(P: np.ndarray, ranks: np.ndarray, ranks_per_node: int, c: float) -> np.ndarray:
+    """Eq. 2-3 objective of each placement row of `ranks`, summed sequentially
+    over i < j in row-major order (so the rounding is the same for every row)."""
+    n = P.shape[0]
+    iu, ju = np.triu_indices(n, 1)
+    pv = P[iu, ju]
+    a, b = ranks[:, iu], ranks[:, ju]
+    dist = np.where(a == b, 0.0, np.where(a // ranks_per_node == b // ranks_per_node, 1.0, float(c)))
+    return np.cumsum(pv[None, :] * dist, axis=1)[:, -1]
+
+
+def adjustment_spectrum(C, expert_rank, expert_local, R: int, ranks_per_node: int, c: float,
+                        max_swaps: int = 1 << 30):
+    """[(expert_rank, expert_local, swapped pair or None)], the starting
+    placement first, then one entry per swap."""
+    P = coactivation_probability(C)
+    N = np.diag(np.asarray(C, dtype=np.int64)).copy()
+    er = np.asarray(expert_rank, dtype=np.int32).copy()
+    el = np.asarray(expert_local, dtype=np.int32).copy()
+    out = [(er.copy(), el.copy(), None)]
+    for _ in range(max_swaps):
+        L = np.bincount(er, weights=N, minlength=R).astype(np.int64)
+        hi = int(np.flatnonzero(L == L.max())[0])
+        lo = int(np.flatnonzero(L == L.min())[0])
+        if L[hi] == L[lo]:
+            break
+        es, fs = np.flatnonzero(er == hi), np.flatnonzero(er == lo)
+        E2, F2 = np.meshgrid(es, fs, indexing="ij")
+        E2, F2 = E2.ravel(), F2.ravel()                     # (e asc, f asc) order
+        ok = (N[E2] > N[F2]) & (L[lo] + N[E2] - N[F2] < L[hi])
+        if not ok.any():
+            break
+        E2, F2 = E2[ok], F2[ok]
+        trial = np.repeat(er[None, :], len(E2), axis=0)
+        rows = np.arange(len(E2))
+        trial[rows, E2] = lo
+        trial[rows, F2] = hi
+        base = _sequential_objectives(P, er[None, :], ranks_per_node, c)[0]
+        delta = _sequential_objectives(P, trial, ranks_per_node, c) - base
+        k = int(np.argmin(delta))                           # first minimum: lower e, then f
+        e, f = int(E2[k]), int(F2[k])
+        er[e], er[f] = lo, hi
+        el[e], el[f] = el[f], el[e]
+        out.append((er.copy(), el.copy(), (e, f)))
+    return out
+
+
+def spectrum_points(n_placements: int, points: int = 7) -> list[int]:
+    """Indices of `points` placements evenly spread over a spectrum of
+    n_placements (first and last included)."""
+    if n_placements <= points:
+        return list(range(n_placements))
+    return sorted({round(i * (n_placements - 1) / (points - 1)) for i in range(points)})
