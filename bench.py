@@ -281,9 +281,9 @@ def main():
     t_start.record(stream)
     for i in range(K):
         L.front()
-        L.gather(rank)
+        L.row_source(rank)
         ffn_ev[i][0].record(stream)
-        L.ffn(rank)
+        L.ffn_gather(rank)
         ffn_ev[i][1].record(stream)
         L.dest_reduce(rank)
         L.shared_ffn(rank)
@@ -296,9 +296,10 @@ def main():
     log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
 
     # per-stage breakdown (separate, untimed pass)
-    stages = ["route", "layout", "coact", "gather", "ffn", "dest", "shared", "src"]
-    fns = [L.route, L.layout, L.coactivation, lambda: L.gather(rank), lambda: L.ffn(rank),
-           lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank)]
+    stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
+    fns = [L.route, L.layout, L.coactivation, lambda: L.row_source(rank), lambda: L.ffn_gather(rank),
+           lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank),
+           lambda: L.gather(rank), lambda: L.ffn(rank)]
     reps = 5
     acc = {s: 0.0 for s in stages}
     for _ in range(reps):
@@ -380,7 +381,7 @@ def main():
             "parallelism": "1 GPU, virtual EP ranks",
         },
         "roofline": {
-            "kernel": "cap_expert_ffn (gate/up GEMM + down GEMM launches), rank 0",
+            "kernel": "cap_expert_ffn_gather (gate/up GEMM reading x rows in place + down GEMM), rank 0",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
             "flops_per_call": flops, "rows": rows, "avg_call_ms": ffn_ms,

@@ -54,7 +54,11 @@ typedef enum {
        (pack + all-to-all + expand collapsed into one gather on one GPU) */
     CAP_PERMUTE_EXPERT_GATHER = 0,
     /* source side: the rank's send buffer, one row per (token, kept device) */
-    CAP_PERMUTE_SEND_PACK = 1
+    CAP_PERMUTE_SEND_PACK = 1,
+    /* destination side, index only: the token each expert-sorted row of the
+       rank comes from (the permutation of EXPERT_GATHER without moving rows;
+       cap_expert_ffn_gather then reads the rows in place) */
+    CAP_PERMUTE_ROW_SOURCE = 2
 } cap_permute_mode;
 
 typedef enum {
@@ -209,6 +213,10 @@ cap_status cap_dispatch_layout(const cap_topology *topo, const int32_t *idx, con
  *       = x[t] for every kept slot on r.  out holds rank r's expert-sorted rows.
  *   CAP_PERMUTE_SEND_PACK, rank s: out[send_offsets[s][d] + j] = x[t] for the
  *       j-th token t of s (ascending) whose mask holds d.
+ *   CAP_PERMUTE_ROW_SOURCE, rank r: out is int32;
+ *       out[slot_pos(t,s) - expert_offsets[r*E_loc]] = t for every kept slot on r,
+ *       i.e. EXPERT_GATHER of the token index instead of the token's row.
+ *       dtype, d and x are not used (x may be NULL); out needs 4-byte alignment.
  * x is [T][d].  The layout arrays come from cap_dispatch_layout.
  * out_rows is the capacity of `out` in rows: rows at or past it are not
  * written (size it with expert_offsets / send_counts, or an upper bound such
@@ -242,6 +250,26 @@ cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t int
                           int32_t max_rows, const void *xs, const int32_t *row_offsets,
                           const void *w1, const void *w3, const void *w2, void *y,
                           void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * cap_expert_ffn with the token permutation folded into the first GEMM's
+ * operand loads (Sec. II-C expansion; Eq. 1): row i of the expert-sorted input
+ * is x[row_src[i]], read in place instead of from a gathered copy.
+ *   x[x_rows][d]      token rows (the rank's received rows on a real system;
+ *                     all T tokens on one GPU).
+ *   row_src[max_rows] (device) source row of each expert-sorted row, e.g. the
+ *                     output of cap_permute(CAP_PERMUTE_ROW_SOURCE).  Entries
+ *                     outside [0, x_rows) are clamped into it (never read out
+ *                     of bounds; such rows are garbage in, garbage out).
+ * Every other argument, the row order of y, the arithmetic and the workspace
+ * are those of cap_expert_ffn, and y is bit-identical to cap_expert_ffn on the
+ * gathered rows.  Needs x_rows >= 1 and x_rows * d * element size < 2^32.
+ */
+cap_status cap_expert_ffn_gather(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter,
+                                 int32_t max_rows, const void *x, int32_t x_rows,
+                                 const int32_t *row_src, const int32_t *row_offsets,
+                                 const void *w1, const void *w3, const void *w2, void *y,
+                                 void *ws, size_t ws_bytes, void *stream);
 
 /*
  * Weighted combine (Sec. II-C local aggregation and final combination; Eq. 1).

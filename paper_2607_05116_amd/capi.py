@@ -6,7 +6,7 @@ fallback: importing this module raises if the library is missing, and every
 call raises CapError on a non-zero status.
 
 Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_dispatch_layout,
-cap_permute, cap_expert_ffn, cap_combine, cap_coactivation,
+cap_permute, cap_expert_ffn, cap_expert_ffn_gather, cap_combine, cap_coactivation,
 cap_workspace_size, cap_status_string, cap_version.
 """
 from __future__ import annotations
@@ -21,13 +21,13 @@ LIB_PATH = os.path.join(_HERE, "libcap.so")
 
 CAP_OK, CAP_ERR_INVALID_ARG, CAP_ERR_UNSUPPORTED, CAP_ERR_WORKSPACE, CAP_ERR_HIP = 0, -1, -2, -3, -4
 CAP_DTYPE_F32, CAP_DTYPE_BF16 = 0, 1
-CAP_PERMUTE_EXPERT_GATHER, CAP_PERMUTE_SEND_PACK = 0, 1
+CAP_PERMUTE_EXPERT_GATHER, CAP_PERMUTE_SEND_PACK, CAP_PERMUTE_ROW_SOURCE = 0, 1, 2
 CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 (CAP_OP_ROUTE_PRUNE, CAP_OP_DISPATCH_LAYOUT, CAP_OP_PERMUTE, CAP_OP_EXPERT_FFN,
  CAP_OP_COMBINE, CAP_OP_COACTIVATION) = range(6)
 
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
-           "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_combine",
+           "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_combine",
            "cap_coactivation"]
 
 
@@ -68,6 +68,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                          vp, i32, vp], ctypes.c_int),
         "cap_expert_ffn": ([ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
                            ctypes.c_int),
+        "cap_expert_ffn_gather": ([ctypes.c_int, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz,
+                                   vp], ctypes.c_int),
         "cap_combine": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, i32, vp, vp, vp, vp,
                          P(Layout), vp, vp, i32, vp], ctypes.c_int),
         "cap_coactivation": ([i32, i32, i32, vp, vp, vp, i32, vp, sz, vp], ctypes.c_int),
@@ -159,6 +161,14 @@ def cap_expert_ffn(dtype, E_loc, d, inter, max_rows, xs, row_offsets, w1, w3, w2
     _check("cap_expert_ffn", _lib.cap_expert_ffn(
         dtype, E_loc, d, inter, max_rows, _ptr(xs), _ptr(row_offsets), _ptr(w1), _ptr(w3), _ptr(w2),
         _ptr(y), _ptr(ws), nbytes, _stream(stream)))
+
+
+def cap_expert_ffn_gather(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2, y, ws,
+                          ws_bytes=None, stream=None):
+    nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
+    _check("cap_expert_ffn_gather", _lib.cap_expert_ffn_gather(
+        dtype, E_loc, d, inter, max_rows, _ptr(x), int(x_rows), _ptr(row_src), _ptr(row_offsets), _ptr(w1),
+        _ptr(w3), _ptr(w2), _ptr(y), _ptr(ws), nbytes, _stream(stream)))
 
 
 def cap_combine(topo, mode, rank, dtype, d, inp, in_rows, idx, w, keep, dst_mask, layout: Layout,

@@ -144,6 +144,16 @@ __device__ __forceinline__ void lds_dma16_clamped(const void* base, uint32_t ld_
                  : "memory");
 }
 
+// Direct load of one 16-byte chunk per lane at base + off + add (a gathered
+// row: off is the lane's row offset plus its chunk, add the stage's K offset).
+__device__ __forceinline__ void lds_dma16_at(const void* base, uint32_t off, uint32_t add, uint32_t lds_addr) {
+    uint32_t v;
+    asm volatile("v_add_u32 %0, %1, %2\n\ts_nop 4\n\tglobal_load_lds_dwordx4 %0, %3"
+                 : "=&v"(v)
+                 : "v"(off), "s"(add), "s"(uniform_ptr(base)), "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
+}
+
 // ------------------------------------------------------------------ bf16 MFMA GEMM
 // LDS holds kStages stages; a stage is the A tile [BM][64] and the B tile
 // [BN][64] (bf16, 128-byte rows).  A stage row is one whole 128-byte line of
@@ -207,11 +217,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 // they write their own outputs and the staged ones, and never wait for
 // stores.  The staging area is stage buffer 1, free from the end of a tile's K
 // loop until the next tile fills its stage 1 (one barrier later).
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool GATEUP>
+//
+// GATHER: row i of A is A[row_src[i]] (A has x_rows rows): each loader lane
+// keeps the byte offsets of the rows it loads for the current tile.
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool GATEUP, bool GATHER>
 __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
     uint16_t* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K,
-    int N_out) {
+    int N_out, const int32_t* __restrict__ row_src, int x_rows) {
     constexpr int NW = WAVES_M * WAVES_N;
     constexpr int NL = NW / 2;                             // loader waves
     constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
@@ -272,7 +285,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     constexpr int B_RUN = GATEUP ? B_LD / 2 : B_LD;        // loads per contiguous B run
     static_assert(!GATEUP || B_RUN * ROWS_PER_LOAD == 32, "a gate/up loader covers one 32-row W1/W3 pair");
     struct TileSrc {
-        const char* a;              // A + row0 * K
+        const char* a;              // A + row0 * K (GATHER: A)
         int a_last;                 // last valid row of the tile
         const char* b[2];           // first row of each B run
     };
@@ -284,7 +297,8 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         const int l = __builtin_amdgcn_readfirstlane(find_expert(mt_prefix, E_loc, m_tile));
         row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (m_tile - mt_prefix[l]) * BM);
         rows_valid = __builtin_amdgcn_readfirstlane(min(BM, row_end[l] - row0));
-        src.a = reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
+        src.a = GATHER ? reinterpret_cast<const char*>(A)
+                       : reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
         src.a_last = rows_valid - 1;
         const int lw = loader ? wave : 0;
         if constexpr (GATEUP) {
@@ -305,6 +319,20 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     const uint32_t pitch = static_cast<uint32_t>(K) * 2u;                 // bytes per operand row
     const uint32_t lane_off[2] = {ld_row * pitch + col_b[0], ld_row * pitch + col_b[1]};
     const uint32_t blk_bytes = static_cast<uint32_t>(ROWS_PER_LOAD) * pitch;
+    // GATHER: byte offset (row and chunk) of each A row this loader lane loads
+    uint32_t a_off[GATHER ? A_LD : 1];
+    auto gather_offsets = [&](int tile_row0, int a_last) {
+        if constexpr (GATHER) {
+            if (!loader) return;
+#pragma unroll
+            for (int i = 0; i < A_LD; ++i) {
+                const int r = min(wave * A_LD * ROWS_PER_LOAD + i * ROWS_PER_LOAD + ld_row, a_last);
+                int tok = row_src[tile_row0 + r];
+                tok = min(max(tok, 0), x_rows - 1);
+                a_off[i] = static_cast<uint32_t>(tok) * pitch + col_b[(wave * A_LD + i) & 1];
+            }
+        }
+    };
     auto issue_stage = [&](const TileSrc& src, int kt) {
         if (!loader) return;
         const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * STAGE_B);
@@ -312,7 +340,11 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         const char* a_base = src.a + kb + static_cast<size_t>(wave * A_LD) * blk_bytes;
         const uint32_t a_lds = st + wave * A_LD * 1024;
         const int a_first = wave * A_LD * ROWS_PER_LOAD;
-        if (a_first + A_LD * ROWS_PER_LOAD - 1 <= src.a_last) {                  // wave-uniform
+        if constexpr (GATHER) {
+            static_for<A_LD>([&](auto I) {
+                lds_dma16_at(src.a, a_off[I.value], static_cast<uint32_t>(kb), a_lds + I.value * 1024);
+            });
+        } else if (a_first + A_LD * ROWS_PER_LOAD - 1 <= src.a_last) {           // wave-uniform
             static_for<A_LD>([&](auto I) {
                 lds_dma16_blk<I.value>(a_base, lane_off[(wave * A_LD + I.value) & 1], blk_bytes, a_lds + I.value * 1024);
             });
@@ -336,6 +368,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
     TileSrc src;
     if (tile < total) {
         src = tile_sources(tile, row0, rows_valid, nt);
+        gather_offsets(row0, src.a_last);
         issue_stage(src, 0);
     }
     while (tile < total) {
@@ -385,6 +418,7 @@ __global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_ke
         const int next = tile + gridDim.x;
         if (next < total) {
             src = tile_sources(next, row0, rows_valid, nt);
+            gather_offsets(row0, src.a_last);
             issue_stage(src, 0);
         }
 
@@ -462,7 +496,8 @@ constexpr int kF32K = 16;
 template <bool GATEUP>
 __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(
     const float* __restrict__ A, const float* __restrict__ B0, const float* __restrict__ B1,
-    float* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K, int N_out) {
+    float* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K, int N_out,
+    const int32_t* __restrict__ row_src, int x_rows) {
     __shared__ float sa[kF32K][kF32Tile + 1];
     __shared__ float sb0[kF32K][kF32Tile + 1];
     __shared__ float sb1[kF32K][kF32Tile + 1];
@@ -485,7 +520,8 @@ __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(
             for (int i = threadIdx.x; i < kF32K * kF32Tile; i += 256) {
                 const int r = i / kF32K, kk = i % kF32K;
                 const int gk = k0 + kk;
-                const int gr = row0 + min(r, rows_valid - 1);
+                int gr = row0 + min(r, rows_valid - 1);
+                if (row_src) gr = min(max(row_src[gr], 0), x_rows - 1);
                 const int gn = nt * kF32Tile + r;
                 sa[kk][r] = gk < K ? A[static_cast<size_t>(gr) * K + gk] : 0.0f;
                 sb0[kk][r] = (gk < K && gn < N_out) ? W0[static_cast<size_t>(gn) * K + gk] : 0.0f;
@@ -547,32 +583,40 @@ cap_status ffn_supported(cap_dtype dt, int d, int inter) {
     return (d % 4 == 0) ? CAP_OK : CAP_ERR_UNSUPPORTED;
 }
 
-cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_rows, const void* xs,
-                             const int32_t* row_offsets, const void* w1, const void* w3, const void* w2,
-                             void* y, void* ws, hipStream_t st) {
+// row_src == nullptr: xs holds the expert-sorted rows; otherwise row i is
+// xs[row_src[i]] and xs has x_rows rows.
+cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_rows, const void* xs, int x_rows,
+                             const int32_t* row_src, const int32_t* row_offsets, const void* w1, const void* w3,
+                             const void* w2, void* y, void* ws, hipStream_t st) {
     if (dt == CAP_DTYPE_BF16) {
         const long long mt_upper = (static_cast<long long>(max_rows) + kBM - 1) / kBM + E_loc;
         const int g1 = persistent_grid(mt_upper * (inter / (kBN / 2)));
-        ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true><<<g1, kWavesM * kWavesN * kWave, 0, st>>>(
-            static_cast<const uint16_t*>(xs), static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3),
-            static_cast<uint16_t*>(ws), row_offsets, E_loc, max_rows, d, inter);
+        const auto* a = static_cast<const uint16_t*>(xs);
+        if (row_src)
+            ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true, true><<<g1, kWavesM * kWavesN * kWave, 0, st>>>(
+                a, static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3), static_cast<uint16_t*>(ws),
+                row_offsets, E_loc, max_rows, d, inter, row_src, x_rows);
+        else
+            ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true, false><<<g1, kWavesM * kWavesN * kWave, 0, st>>>(
+                a, static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3), static_cast<uint16_t*>(ws),
+                row_offsets, E_loc, max_rows, d, inter, nullptr, 0);
         CAP_LAUNCH_CHECK();
         const int g2 = persistent_grid(mt_upper * (d / kBN));
-        ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, false><<<g2, kWavesM * kWavesN * kWave, 0, st>>>(
+        ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, false, false><<<g2, kWavesM * kWavesN * kWave, 0, st>>>(
             static_cast<const uint16_t*>(ws), static_cast<const uint16_t*>(w2), nullptr,
-            static_cast<uint16_t*>(y), row_offsets, E_loc, max_rows, inter, d);
+            static_cast<uint16_t*>(y), row_offsets, E_loc, max_rows, inter, d, nullptr, 0);
         CAP_LAUNCH_CHECK();
     } else {
         const long long mt_upper = (static_cast<long long>(max_rows) + kF32Tile - 1) / kF32Tile + E_loc;
         const int g1 = persistent_grid(mt_upper * ((inter + kF32Tile - 1) / kF32Tile)) * 4;
         ffn_gemm_f32_kernel<true><<<g1, 256, 0, st>>>(
             static_cast<const float*>(xs), static_cast<const float*>(w1), static_cast<const float*>(w3),
-            static_cast<float*>(ws), row_offsets, E_loc, max_rows, d, inter);
+            static_cast<float*>(ws), row_offsets, E_loc, max_rows, d, inter, row_src, x_rows);
         CAP_LAUNCH_CHECK();
         const int g2 = persistent_grid(mt_upper * ((d + kF32Tile - 1) / kF32Tile)) * 4;
         ffn_gemm_f32_kernel<false><<<g2, 256, 0, st>>>(
             static_cast<const float*>(ws), static_cast<const float*>(w2), nullptr, static_cast<float*>(y),
-            row_offsets, E_loc, max_rows, inter, d);
+            row_offsets, E_loc, max_rows, inter, d, nullptr, 0);
         CAP_LAUNCH_CHECK();
     }
     return CAP_OK;

@@ -156,6 +156,30 @@ __global__ __launch_bounds__(kThreads) void expert_gather_kernel(
     }
 }
 
+// ---------------------------------------------------------------- row source
+// Index-only expert gather: one thread per (received token, slot) writes the
+// token index into the slot's expert-sorted row.
+__global__ __launch_bounds__(kThreads) void row_source_kernel(
+    Topo g, int rank, const int32_t* __restrict__ slot_pos, const int32_t* __restrict__ expert_offsets,
+    const int32_t* __restrict__ recv_offsets, const int32_t* __restrict__ recv_token, int32_t* __restrict__ out,
+    int out_rows) {
+    const int r0 = recv_offsets[rank];
+    if (r0 < 0) return;
+    const int U = min(recv_offsets[rank + 1] - r0, g.T * g.k - r0);
+    const int base = expert_offsets[rank * g.E_loc];
+    const int rows_r = min(expert_offsets[(rank + 1) * g.E_loc] - base, out_rows);
+    const long long items = static_cast<long long>(U) * g.k;
+    for (long long i = static_cast<long long>(blockIdx.x) * kThreads + threadIdx.x; i < items;
+         i += static_cast<long long>(gridDim.x) * kThreads) {
+        const int u = static_cast<int>(i / g.k);
+        const int s = static_cast<int>(i - static_cast<long long>(u) * g.k);
+        const int t = recv_token[r0 + u];
+        if (static_cast<unsigned>(t) >= static_cast<unsigned>(g.T)) continue;
+        const int rr = slot_pos[static_cast<size_t>(t) * g.k + s] - base;
+        if (static_cast<unsigned>(rr) < static_cast<unsigned>(rows_r)) out[rr] = t;
+    }
+}
+
 // ---------------------------------------------------------------- send pack
 template <int JB>
 __global__ __launch_bounds__(kThreads) void send_pack_kernel(
@@ -415,6 +439,17 @@ cap_status permute_launch(const cap_topology* tp, cap_permute_mode mode, int ran
                           const void* x, const int32_t* idx, const uint8_t* keep, const uint64_t* mask,
                           const cap_layout* lay, void* out, int out_rows, hipStream_t st) {
     const Topo g = make_topo(tp);
+    if (mode == CAP_PERMUTE_ROW_SOURCE) {
+        const long long items = static_cast<long long>(g.T) * g.k;
+        long long grid = (items + kThreads - 1) / kThreads;
+        const long long cap = static_cast<long long>(device_cu_count()) * 8;
+        grid = grid < 1 ? 1 : (grid < cap ? grid : cap);
+        row_source_kernel<<<static_cast<int>(grid), kThreads, 0, st>>>(
+            g, rank, lay->slot_pos, lay->expert_offsets, lay->recv_offsets, lay->recv_token,
+            static_cast<int32_t*>(out), out_rows);
+        CAP_LAUNCH_CHECK();
+        return CAP_OK;
+    }
     const int row_bytes = d * (dt == CAP_DTYPE_BF16 ? 2 : 4);
     const int vpr = row_bytes / 16;
     const u32x4* xv = static_cast<const u32x4*>(x);

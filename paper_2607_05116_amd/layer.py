@@ -74,6 +74,7 @@ class DeviceLayer:
         self.row_cap = row_cap if row_cap is not None else T * min(k, cfg.E_loc)
         self.recv_cap = recv_cap if recv_cap is not None else T * min(k, R)
         self.xs = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
+        self.row_src = torch.empty(self.row_cap, **i32)
         self.Y = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
         self.parts = torch.zeros((self.recv_cap, d), dtype=self.tdt, device=self.dev)
         self.y = torch.empty((cfg.tokens_per_rank, d), dtype=self.tdt, device=self.dev)
@@ -81,6 +82,7 @@ class DeviceLayer:
                                                        self.row_cap, self.dt))
         self.weights: dict[int, tuple] = {}
         self.naive = False              # expert-level threshold pruning instead of CAP's
+        self.fused_gather = True        # FFN reads x through row_src instead of a gathered copy
         self.shared = None
         self.shared_out = None
         self.ws_shared = None
@@ -126,6 +128,10 @@ class DeviceLayer:
         capi.cap_permute(self.topo, capi.CAP_PERMUTE_EXPERT_GATHER, rank, self.dt, self.d, self.x,
                          self.idx, self.keep, self.mask, self.lay, self.xs, self.row_cap, stream)
 
+    def row_source(self, rank: int, stream=None):
+        capi.cap_permute(self.topo, capi.CAP_PERMUTE_ROW_SOURCE, rank, self.dt, self.d, None,
+                         self.idx, self.keep, self.mask, self.lay, self.row_src, self.row_cap, stream)
+
     def send_pack(self, rank: int, out: torch.Tensor, stream=None):
         capi.cap_permute(self.topo, capi.CAP_PERMUTE_SEND_PACK, rank, self.dt, self.d, self.x,
                          self.idx, self.keep, self.mask, self.lay, out, out.shape[0], stream)
@@ -136,6 +142,15 @@ class DeviceLayer:
         offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
         capi.cap_expert_ffn(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.xs, offs,
                             w1, w3, w2, self.Y, self.ws_ffn, stream=stream)
+
+    def ffn_gather(self, rank: int, stream=None):
+        """The rank's expert FFN reading its rows from x through row_src."""
+        w1, w3, w2 = self.weights[rank]
+        E_loc = self.cfg.E_loc
+        offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
+        capi.cap_expert_ffn_gather(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.x,
+                                   self.x.shape[0], self.row_src, offs, w1, w3, w2, self.Y, self.ws_ffn,
+                                   stream=stream)
 
     def shared_ffn(self, rank: int, stream=None):
         if self.shared is None:
@@ -165,8 +180,12 @@ class DeviceLayer:
 
     def rank_path(self, rank: int, stream=None):
         """The destination and source work of one rank."""
-        self.gather(rank, stream)
-        self.ffn(rank, stream)
+        if self.fused_gather:
+            self.row_source(rank, stream)
+            self.ffn_gather(rank, stream)
+        else:
+            self.gather(rank, stream)
+            self.ffn(rank, stream)
         self.dest_reduce(rank, stream)
         self.shared_ffn(rank, stream)
         self.src_reduce(rank, stream)

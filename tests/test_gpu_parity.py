@@ -190,6 +190,78 @@ def test_permute_exact(name, kind, p):
         assert np.array_equal(got.view(np.uint8), want.view(np.uint8)), rank
 
 
+@pytest.mark.parametrize("case", C.ROUTE_CASES, ids=lambda c: c.id)
+def test_row_source_bit_exact(case):
+    """CAP_PERMUTE_ROW_SOURCE is the expert gather of the token index."""
+    cfg = case.cfg
+    L = _layer(case)
+    L.front()
+    r, lay = C.oracle_routing(case.name, case.placement, case.p, case.c)
+    er, _ = C.placement(case.name, case.placement, case.p, case.c)
+    tok = np.arange(cfg.T, dtype=np.int32)[:, None]
+    for rank in sorted({0, cfg.R - 1}):
+        L.row_source(rank)
+        torch.cuda.synchronize()
+        want = oracle.expert_gather(tok, r["idx"], r["keep"], lay["slot_pos"], lay["expert_offsets"], er, cfg.R,
+                                    rank)[:, 0]
+        got = L.row_src[: len(want)].cpu().numpy()
+        assert np.array_equal(got, want), rank
+
+
+@pytest.mark.parametrize("name,kind,p", [("c1", "seq", 0.3), ("c2", "coact", 0.3), ("c4", "coact", 0.1),
+                                         ("c5", "coact", 0.1)])
+def test_ffn_gather_equals_ffn_on_gathered_rows(name, kind, p):
+    """Reading x through row_src gives the same bits as the FFN on the gathered copy."""
+    case = C.Case(name, gen.CONFIGS[name], kind, p)
+    cfg = case.cfg
+    er, el = C.placement(name, kind, p, 5.0)
+    L = _layer(case, x=gen.activations(cfg))
+    for rank in sorted({0, cfg.R - 1}):
+        L.set_rank_weights(rank, *C.rank_weights(cfg, er, el, rank))
+        L.front()
+        L.gather(rank)
+        L.ffn(rank)
+        torch.cuda.synchronize()
+        rows = L.rank_rows(rank)
+        want = L.Y[:rows].clone()
+        L.Y.zero_()
+        L.row_source(rank)
+        L.ffn_gather(rank)
+        torch.cuda.synchronize()
+        assert torch.equal(L.Y[:rows].view(torch.uint8), want.view(torch.uint8)), rank
+        del L.weights[rank]
+
+
+@pytest.mark.parametrize("dtype,d,inter,counts", [("bf16", 512, 384, [300, 1, 0, 513]),
+                                                  ("bf16", 256, 128, [0, 700, 40]),
+                                                  ("f32", 128, 256, [70, 0, 131])])
+def test_ffn_gather_ragged_with_repeats_and_clamping(dtype, d, inter, counts):
+    """Ragged experts, repeated source rows and out-of-range indices (clamped
+    into [0, x_rows)) against cap_expert_ffn on the explicitly gathered rows."""
+    rng = np.random.default_rng(len(counts) + d)
+    E_loc, rows = len(counts), int(sum(counts))
+    offs = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32) + 9).cuda()
+    x_rows = 97
+    max_rows = rows + 3
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    cdt = capi.CAP_DTYPE_BF16 if dtype == "bf16" else capi.CAP_DTYPE_F32
+    x = torch.from_numpy(rng.standard_normal((x_rows, d)).astype(np.float32)).to(tdt).cuda()
+    src = rng.integers(-3, x_rows + 3, size=max_rows).astype(np.int32)
+    row_src = torch.from_numpy(src).cuda()
+    xs = x[torch.from_numpy(np.clip(src, 0, x_rows - 1).astype(np.int64)).cuda()].contiguous()
+    w1 = (torch.randn(E_loc, inter, d, device="cuda") / d ** 0.5).to(tdt)
+    w3 = (torch.randn(E_loc, inter, d, device="cuda") / d ** 0.5).to(tdt)
+    w2 = (torch.randn(E_loc, d, inter, device="cuda") / (12 * inter ** 0.5)).to(tdt)
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                     dtype=torch.uint8, device="cuda")
+    y_ref = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
+    y = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
+    capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, xs, offs, w1, w3, w2, y_ref, ws)
+    capi.cap_expert_ffn_gather(cdt, E_loc, d, inter, max_rows, x, x_rows, row_src, offs, w1, w3, w2, y, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y[:rows].view(torch.uint8), y_ref[:rows].view(torch.uint8))
+
+
 # ---------------------------------------------------------------- expert FFN
 def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0):
     """cap_expert_ffn on synthetic ragged experts; returns (gpu Y, oracle Y)."""

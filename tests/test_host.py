@@ -99,6 +99,21 @@ def test_ffn_rejects_unsupported_shapes(capi):
     assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 0, 2048, 768, 100, *args) == capi.CAP_ERR_INVALID_ARG
 
 
+def test_ffn_gather_validation(capi):
+    f = capi._lib.cap_expert_ffn_gather
+    B = capi.CAP_DTYPE_BF16
+    ws = 1 << 30
+    ok = (0x1000, 512, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, 0x7000, 0x8000, ws, None)
+    assert f(B, 4, 2048, 768, 100, None, *ok[1:]) == capi.CAP_ERR_INVALID_ARG             # x
+    assert f(B, 4, 2048, 768, 100, 0x1000, 512, None, *ok[3:]) == capi.CAP_ERR_INVALID_ARG  # row_src
+    assert f(B, 4, 2048, 768, 100, 0x1000, 0, *ok[2:]) == capi.CAP_ERR_INVALID_ARG         # x_rows
+    assert f(B, 4, 2000, 768, 100, *ok) == capi.CAP_ERR_UNSUPPORTED                         # d
+    big = (0x1000, (1 << 32) // 4096) + ok[2:]
+    assert f(B, 4, 2048, 768, 100, *big) == capi.CAP_ERR_UNSUPPORTED                        # 32-bit offsets
+    small_ws = ok[:-2] + (100 * 768 * 2 - 1, None)
+    assert f(B, 4, 2048, 768, 100, *small_ws) == capi.CAP_ERR_WORKSPACE
+
+
 def test_permute_and_combine_validation(capi):
     t = _topo(capi)
     lay = capi.Layout(*([0x10000] * 10))
@@ -111,6 +126,15 @@ def test_permute_and_combine_validation(capi):
     bad_d = capi._lib.cap_permute(ctypes.byref(t), 0, 0, 1, 12, 0x1000, 0x2000, 0x3000, 0x4000,
                                   ctypes.byref(lay), 0x5000, 10, None)
     assert bad_d == capi.CAP_ERR_INVALID_ARG
+    no_x = capi._lib.cap_permute(ctypes.byref(t), 0, 0, 1, 128, None, 0x2000, 0x3000, 0x4000,
+                                 ctypes.byref(lay), 0x5000, 10, None)
+    assert no_x == capi.CAP_ERR_INVALID_ARG
+    rs_bad_rank = capi._lib.cap_permute(ctypes.byref(t), capi.CAP_PERMUTE_ROW_SOURCE, 4, 1, 0, None, 0x2000,
+                                        0x3000, 0x4000, ctypes.byref(lay), 0x5000, 10, None)
+    assert rs_bad_rank == capi.CAP_ERR_INVALID_ARG
+    rs_misaligned = capi._lib.cap_permute(ctypes.byref(t), capi.CAP_PERMUTE_ROW_SOURCE, 0, 1, 0, None, 0x2000,
+                                          0x3000, 0x4000, ctypes.byref(lay), 0x5002, 10, None)
+    assert rs_misaligned == capi.CAP_ERR_INVALID_ARG
     small_out = capi._lib.cap_combine(ctypes.byref(t), 1, 0, 1, 128, 0x1000, 10, 0x2000, 0x3000, 0x4000,
                                       0x5000, ctypes.byref(lay), None, 0x6000, 63, None)
     assert small_out == capi.CAP_ERR_INVALID_ARG
