@@ -269,8 +269,24 @@ def main():
     log(f"setup {time.perf_counter() - t_setup:.1f} s; rank-{rank} rows {L.rank_rows(rank)}, received rows {n_recv}")
 
     stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream()            # co-activation beside the layout (default priority)
+
+    def one_step(ev=None):
+        """The whole hot path once: front end over all tokens, then rank r's
+        row source, gathered FFN, destination reduce, shared FFN, source reduce."""
+        L.front(side=side)
+        L.row_source(rank)
+        if ev is not None:
+            ev[0].record(stream)
+        L.ffn_gather(rank)
+        if ev is not None:
+            ev[1].record(stream)
+        L.dest_reduce(rank)
+        L.shared_ffn(rank)
+        L.src_reduce(rank)
+
     for _ in range(args.warmup):
-        L.step(rank)
+        one_step()
     torch.cuda.synchronize()
 
     K = args.steps
@@ -280,14 +296,7 @@ def main():
     wall0 = time.perf_counter()
     t_start.record(stream)
     for i in range(K):
-        L.front()
-        L.row_source(rank)
-        ffn_ev[i][0].record(stream)
-        L.ffn_gather(rank)
-        ffn_ev[i][1].record(stream)
-        L.dest_reduce(rank)
-        L.shared_ffn(rank)
-        L.src_reduce(rank)
+        one_step(ffn_ev[i])
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0

@@ -172,11 +172,25 @@ class DeviceLayer:
                          self.shared_out if self.shared is not None else None, self.y,
                          self.y.shape[0], stream)
 
-    def front(self, stream=None):
-        """Routing front end over all virtual ranks' tokens."""
+    def front(self, stream=None, side=None):
+        """Routing front end over all virtual ranks' tokens.  With a side
+        stream, the co-activation counts (which only feed placement) run there
+        beside the layout; the main stream waits for them before returning
+        control to later work."""
         self.route(stream)
-        self.layout(stream)
-        self.coactivation(False, stream)
+        if side is None:
+            self.layout(stream)
+            self.coactivation(False, stream)
+            return
+        main = stream if stream is not None else torch.cuda.current_stream()
+        if not hasattr(self, "_fork"):
+            self._fork, self._join = torch.cuda.Event(), torch.cuda.Event()
+        self._fork.record(main)
+        side.wait_event(self._fork)
+        self.coactivation(False, side)
+        self._join.record(side)
+        self.layout(main)
+        main.wait_event(self._join)
 
     def rank_path(self, rank: int, stream=None):
         """The destination and source work of one rank."""

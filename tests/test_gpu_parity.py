@@ -91,6 +91,23 @@ def test_coactivation_accumulate():
     assert np.array_equal(L.host("coact").view(np.uint32), 2 * coact)
 
 
+@pytest.mark.parametrize("case", C.ROUTE_CASES[:3], ids=lambda c: c.id)
+def test_front_with_side_stream_matches_serial(case):
+    """Co-activation on a side stream (beside the layout) gives the same bits."""
+    L = _layer(case)
+    L.front()
+    torch.cuda.synchronize()
+    want = {n: L.host(n).copy() for n in ("coact", "slot_pos", "expert_offsets", "totals", "copy_row")}
+    L.coact.zero_()
+    L.lay_t["slot_pos"].fill_(-7)
+    side = torch.cuda.Stream()
+    for _ in range(2):
+        L.front(side=side)
+    torch.cuda.synchronize()
+    for n, v in want.items():
+        assert np.array_equal(L.host(n), v), n
+
+
 def _adversarial_logits(T, E, seed):
     rng = np.random.default_rng(seed)
     L = rng.standard_normal((T, E)).astype(np.float32)
