@@ -134,6 +134,40 @@ def placement_spectrum(L, cfg, C, er, el, c):
     return {"total_swaps": len(spec) - 1, "points": points, "sequential": seq}
 
 
+def fused_front_end(L, cfg, stream, reps=20):
+    """The router GEMM x W_g^T fused with routing and pruning
+    (cap_router_route_prune), timed against the logits-in route kernel
+    (untimed by the step; seeded router weights, so its routing differs from
+    the step's).  Leaves the layer's routing state as the step left it."""
+    import torch
+    from paper_2607_05116_amd.layer import to_device_rows
+    from workloads import generator as gen
+    if cfg.dtype != "bf16":
+        return None
+    wg = to_device_rows(gen.router_weights(cfg), "bf16", L.dev)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    fused_ms = timed(lambda: L.router_route(wg))
+    route_ms = timed(L.route)
+    L.layout()
+    torch.cuda.synchronize()
+    x_bytes = cfg.T * cfg.d * 2 + cfg.E * cfg.d * 2 + cfg.T * cfg.k * 9 + cfg.T * 8
+    return {"router_route_ms": fused_ms, "route_from_logits_ms": route_ms,
+            "router_flops": 2.0 * cfg.T * cfg.d * cfg.E,
+            "router_route_hbm_GBs": x_bytes / (fused_ms * 1e-3) / 1e9,
+            "logits_bytes_not_written": cfg.T * cfg.E * 4}
+
+
 def file_hash(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -366,6 +400,8 @@ def main():
         spectrum = placement_spectrum(L, cfg, coact_counts, er, el, args.c)
         log(f"placement spectrum: {spectrum['total_swaps']} swaps, {time.perf_counter() - t_spec:.1f} s")
 
+    front_end = fused_front_end(L, cfg, stream)
+
     result = {
         "metric": METRIC,
         "value": cfg.tokens_per_rank / (ms_per_step * 1e-3),
@@ -406,6 +442,7 @@ def main():
             "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
             "pruning_cap_vs_naive": pruning,
             "placement_spectrum": spectrum,
+            "fused_router_front_end": front_end,
             "rank_rows": rows, "rank_received_tokens": U,
             "host_wall_ms_per_step": 1e3 * wall / K,
         },

@@ -198,6 +198,24 @@ cap_status cap_route_prune_naive(const cap_topology *topo, const float *logits, 
                                  void *stream);
 
 /*
+ * Router GEMM fused with cap_route_prune (Eq. 1: the gate takes the top k of
+ * the router logits x W_g^T; Sec. VI, Eq. 6 pruning).  The fp32 logits of each
+ * group of 64 or 128 tokens are computed on the matrix cores into on-chip memory
+ * and routed from there; the outputs are those of cap_route_prune on the same
+ * logits, bit for bit.
+ *   dtype            CAP_DTYPE_BF16 only (x and w_gate bf16, fp32 accumulation
+ *                    in K order per 16-wide step).
+ *   x[T][d]          token activations; w_gate[E][d] router weights (row e
+ *                    gives expert e's logit); both 16-byte aligned.
+ *   logits[T][E]     optional (NULL: not written) fp32 logits the routing used.
+ * Other arguments as cap_route_prune.  Needs d % 64 == 0 and 16 < E <= 256
+ * (CAP_ERR_UNSUPPORTED otherwise).  No workspace.
+ */
+cap_status cap_router_route_prune(const cap_topology *topo, cap_dtype dtype, int32_t d, const void *x,
+                                  const void *w_gate, float p, int32_t *idx, float *w, uint8_t *keep,
+                                  uint64_t *dst_mask, float *logits, void *stream);
+
+/*
  * Counting and prefix scans into the all-to-all send layout, the expert-sorted
  * layout and per-token send volume (Sec. II-C device-centric transfer; Eq. 3
  * topology classes).  Inputs: the outputs of cap_route_prune.  Outputs: every

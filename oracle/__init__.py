@@ -117,6 +117,11 @@ def prune_naive(idx, w, expert_rank, p):
     return keep, wp, mask
 
 
+def router_logits(x, w_gate) -> np.ndarray:
+    """Router logits of Eq. 1, x W_g^T, in fp64 (x [T][d], w_gate [E][d])."""
+    return np.asarray(x, np.float64) @ np.asarray(w_gate, np.float64).T
+
+
 def route_prune(logits, k, expert_rank, ranks_per_node, tokens_per_rank, c, p):
     """Top-k, gates, then communication-aware pruning (the paper's order)."""
     idx = topk(logits, k)

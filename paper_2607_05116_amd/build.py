@@ -36,6 +36,7 @@ CXXFLAGS = [
 # through the long compare/select networks of the top-k (minutes -> seconds).
 FILE_FLAGS = {
     "route_prune.hip": ["-fno-honor-nans"],
+    "router_route.hip": ["-fno-honor-nans"],
 }
 
 

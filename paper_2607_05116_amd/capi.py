@@ -5,7 +5,8 @@ every computation runs in the HIP kernels of libcap.so.  There is no CPU
 fallback: importing this module raises if the library is missing, and every
 call raises CapError on a non-zero status.
 
-Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_dispatch_layout,
+Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_router_route_prune,
+cap_dispatch_layout,
 cap_permute, cap_expert_ffn, cap_expert_ffn_gather, cap_combine, cap_coactivation,
 cap_workspace_size, cap_status_string, cap_version.
 """
@@ -27,6 +28,7 @@ CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
  CAP_OP_COMBINE, CAP_OP_COACTIVATION) = range(6)
 
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
+           "cap_router_route_prune",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_combine",
            "cap_coactivation"]
 
@@ -63,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "cap_workspace_size": ([ctypes.c_int, P(Topology), i32, i32, i32, ctypes.c_int], sz),
         "cap_route_prune": ([P(Topology), vp, f32, vp, vp, vp, vp, vp], ctypes.c_int),
         "cap_route_prune_naive": ([P(Topology), vp, f32, vp, vp, vp, vp, vp], ctypes.c_int),
+        "cap_router_route_prune": ([P(Topology), ctypes.c_int, i32, vp, vp, f32, vp, vp, vp, vp, vp, vp],
+                                   ctypes.c_int),
         "cap_dispatch_layout": ([P(Topology), vp, vp, vp, P(Layout), vp, sz, vp], ctypes.c_int),
         "cap_permute": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, vp, vp, vp, P(Layout),
                          vp, i32, vp], ctypes.c_int),
@@ -139,6 +143,12 @@ def cap_route_prune(topo, logits, p, idx, w, keep, dst_mask, stream=None):
     _check("cap_route_prune", _lib.cap_route_prune(
         ctypes.byref(topo), _ptr(logits), float(p), _ptr(idx), _ptr(w), _ptr(keep), _ptr(dst_mask),
         _stream(stream)))
+
+
+def cap_router_route_prune(topo, dtype, d, x, w_gate, p, idx, w, keep, dst_mask, logits=None, stream=None):
+    _check("cap_router_route_prune", _lib.cap_router_route_prune(
+        ctypes.byref(topo), dtype, int(d), _ptr(x), _ptr(w_gate), float(p), _ptr(idx), _ptr(w), _ptr(keep),
+        _ptr(dst_mask), _ptr(logits), _stream(stream)))
 
 
 def cap_dispatch_layout(topo, idx, keep, dst_mask, layout: Layout, ws, ws_bytes=None, stream=None):

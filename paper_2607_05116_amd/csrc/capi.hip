@@ -9,6 +9,9 @@ namespace cap {
 
 cap_status route_prune_launch(const cap_topology*, const float*, float, bool, int32_t*, float*, uint8_t*, uint64_t*,
                               hipStream_t);
+bool router_route_supported(const cap_topology*, int);
+cap_status router_route_launch(const cap_topology*, int, const void*, const void*, float, int32_t*, float*, uint8_t*,
+                               uint64_t*, float*, hipStream_t);
 size_t layout_workspace_bytes(const cap_topology*);
 cap_status dispatch_layout_launch(const cap_topology*, const int32_t*, const uint8_t*, const uint64_t*,
                                   const cap_layout*, void*, hipStream_t);
@@ -116,6 +119,17 @@ cap_status cap_route_prune_naive(const cap_topology* topo, const float* logits, 
     if (!topo_ok(topo) || !logits || !idx || !w || !keep || !dst_mask) return CAP_ERR_INVALID_ARG;
     if (!(p >= 0.0f) || !(p < 1.0f)) return CAP_ERR_INVALID_ARG;
     return route_prune_launch(topo, logits, p, true, idx, w, keep, dst_mask, as_stream(stream));
+}
+
+cap_status cap_router_route_prune(const cap_topology* topo, cap_dtype dtype, int32_t d, const void* x,
+                                  const void* w_gate, float p, int32_t* idx, float* w, uint8_t* keep,
+                                  uint64_t* dst_mask, float* logits, void* stream) {
+    if (!topo_ok(topo) || !x || !w_gate || !idx || !w || !keep || !dst_mask) return CAP_ERR_INVALID_ARG;
+    if (!(p >= 0.0f) || !(p < 1.0f) || d < 1) return CAP_ERR_INVALID_ARG;
+    if (dtype != CAP_DTYPE_BF16 || !router_route_supported(topo, d)) return CAP_ERR_UNSUPPORTED;
+    if (!aligned16(x) || !aligned16(w_gate) || (reinterpret_cast<uintptr_t>(logits) & 3) != 0)
+        return CAP_ERR_INVALID_ARG;
+    return router_route_launch(topo, d, x, w_gate, p, idx, w, keep, dst_mask, logits, as_stream(stream));
 }
 
 cap_status cap_dispatch_layout(const cap_topology* topo, const int32_t* idx, const uint8_t* keep,

@@ -116,6 +116,11 @@ class DeviceLayer:
         fn = capi.cap_route_prune_naive if self.naive else capi.cap_route_prune
         fn(self.topo, self.logits, self.p, self.idx, self.w, self.keep, self.mask, stream)
 
+    def router_route(self, w_gate: torch.Tensor, logits_out: torch.Tensor | None = None, stream=None):
+        """Router GEMM x W_g^T fused with top-k routing and pruning (bf16 x)."""
+        capi.cap_router_route_prune(self.topo, self.dt, self.d, self.x, w_gate, self.p, self.idx, self.w,
+                                    self.keep, self.mask, logits_out, stream)
+
     def layout(self, stream=None):
         capi.cap_dispatch_layout(self.topo, self.idx, self.keep, self.mask, self.lay, self.ws_layout,
                                  stream=stream)

@@ -108,6 +108,62 @@ def test_front_with_side_stream_matches_serial(case):
         assert np.array_equal(L.host(n), v), n
 
 
+def _check_router_route(L, cfg, x_bits, wg_bits, er, rows=None):
+    """Fused router + routing: the decisions equal the logits-in kernel's (and
+    the oracle's) on the logits the fused kernel used, and those logits equal
+    x W_g^T within the fp32 accumulation bound d * 2^-24 * sum |x_k w_k|."""
+    from paper_2607_05116_amd.layer import to_device_rows
+    wg = to_device_rows(wg_bits, "bf16", "cuda")
+    lg = torch.empty((cfg.T, cfg.E), dtype=torch.float32, device="cuda")
+    L.router_route(wg, lg)
+    torch.cuda.synchronize()
+    fused = {n: L.host(n).copy() for n in ("idx", "w", "keep", "mask")}
+    L.logits.copy_(lg)
+    L.route()
+    torch.cuda.synchronize()
+    for n, v in fused.items():
+        assert np.array_equal(L.host(n).view(np.uint8), v.view(np.uint8)), n
+    lg_h = lg.cpu().numpy()
+    r = oracle.route_prune(lg_h, cfg.k, er, cfg.ranks_per_node, cfg.tokens_per_rank, L.topo.inter_node_cost,
+                           L.p)
+    assert np.array_equal(fused["idx"], r["idx"])
+    assert np.array_equal(fused["w"].view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(fused["mask"].view(np.uint64), r["mask"])
+    rows = np.arange(cfg.T) if rows is None else rows
+    xf = gen.bf16_bits_to_f32(x_bits[rows]).astype(np.float64)
+    wf = gen.bf16_bits_to_f32(wg_bits).astype(np.float64)
+    ref = oracle.router_logits(xf, wf)
+    bound = cfg.d * 2.0 ** -24 * (np.abs(xf) @ np.abs(wf).T)
+    err = np.abs(lg_h[rows].astype(np.float64) - ref)
+    assert np.all(err <= bound), float((err / np.maximum(bound, 1e-300)).max())
+
+
+@pytest.mark.parametrize("name,kind,p", [("c2", "coact", 0.3), ("c3", "seq", 0.1), ("c4", "coact", 0.1),
+                                         ("c5", "coact", 0.1)])
+def test_router_route_fused(name, kind, p):
+    cfg = gen.CONFIGS[name]
+    er, el = C.placement(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = DeviceLayer(cfg, np.zeros((cfg.T, cfg.E), np.float32), x, er, el, p, 5.0, row_cap=8, recv_cap=8)
+    rows = np.random.default_rng(3).choice(cfg.T, size=4096, replace=False) if cfg.d * cfg.E > 2 ** 20 else None
+    _check_router_route(L, cfg, x, gen.router_weights(cfg), er, rows)
+
+
+@pytest.mark.parametrize("T,E,k,R,rpn,d,p", [(1000, 40, 3, 8, 4, 192, 0.2), (264, 256, 8, 8, 8, 128, 0.3),
+                                             (130, 24, 2, 2, 2, 64, 0.0), (4096, 64, 6, 8, 8, 2048, 0.1)])
+def test_router_route_odd_shapes(T, E, k, R, rpn, d, p):
+    """Ragged token tails, E not a power of two times 8, k = 2..8."""
+    cfg = gen.Config("rt", T=T, d=d, E=E, k=k, inter=128, R=R, ranks_per_node=rpn, n_clusters=1,
+                     zipf_s=0.0, dtype="bf16")
+    rng = np.random.default_rng(T + E)
+    x = gen.f32_to_bf16_bits(rng.standard_normal((T, d)).astype(np.float32))
+    wg = gen.f32_to_bf16_bits((rng.standard_normal((E, d)) / np.sqrt(d)).astype(np.float32))
+    perm = rng.permutation(E)
+    er, el = (perm // (E // R)).astype(np.int32), (perm % (E // R)).astype(np.int32)
+    L = DeviceLayer(cfg, np.zeros((T, E), np.float32), x, er, el, p, 5.0, row_cap=8, recv_cap=8)
+    _check_router_route(L, cfg, x, wg, er)
+
+
 def _adversarial_logits(T, E, seed):
     rng = np.random.default_rng(seed)
     L = rng.standard_normal((T, E)).astype(np.float32)

@@ -76,6 +76,20 @@ def test_route_prune_rejects_null_and_bad_cost(capi, fn):
     assert f(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, None) == -1
 
 
+def test_router_route_validation(capi):
+    f = capi._lib.cap_router_route_prune
+    B, F = capi.CAP_DTYPE_BF16, capi.CAP_DTYPE_F32
+    out = (0x4000, 0x5000, 0x6000, 0x7000, None, None)
+    t = _topo(capi, E=32, R=4)
+    assert f(ctypes.byref(t), F, 128, 0x1000, 0x2000, 0.3, *out) == capi.CAP_ERR_UNSUPPORTED     # dtype
+    assert f(ctypes.byref(t), B, 96, 0x1000, 0x2000, 0.3, *out) == capi.CAP_ERR_UNSUPPORTED      # d % 64
+    assert f(ctypes.byref(t), B, 128, None, 0x2000, 0.3, *out) == capi.CAP_ERR_INVALID_ARG       # x
+    assert f(ctypes.byref(t), B, 128, 0x1008, 0x2000, 0.3, *out) == capi.CAP_ERR_INVALID_ARG     # alignment
+    assert f(ctypes.byref(t), B, 128, 0x1000, 0x2000, 1.0, *out) == capi.CAP_ERR_INVALID_ARG     # p
+    small = _topo(capi, E=16, R=4)
+    assert f(ctypes.byref(small), B, 128, 0x1000, 0x2000, 0.3, *out) == capi.CAP_ERR_UNSUPPORTED  # E <= 16
+
+
 def test_workspace_checks(capi):
     t = _topo(capi)
     need = capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, t)

@@ -262,3 +262,19 @@ def test_naive_pruning_keeps_prefix(orc):
             for v in w[t, :n - 1]:
                 cum = np.float32(cum + v)
             assert cum < np.float32(0.7)
+
+
+def test_router_logits_definition(orc):
+    """x W_g^T: explicit dot products (exact sums), and identity rows pick columns."""
+    import fractions
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((5, 7)).astype(np.float32)
+    wg = rng.standard_normal((3, 7)).astype(np.float32)
+    got = orc.router_logits(x, wg)
+    assert got.shape == (5, 3)
+    for t in range(5):
+        for e in range(3):
+            exact = sum(fractions.Fraction(float(x[t, q])) * fractions.Fraction(float(wg[e, q])) for q in range(7))
+            assert abs(got[t, e] - float(exact)) <= 1e-12
+    eye = np.eye(7, dtype=np.float32)[[4, 0, 6]]
+    assert np.array_equal(orc.router_logits(x, eye), x[:, [4, 0, 6]].astype(np.float64))

@@ -251,6 +251,12 @@ def random_order(n: int, seed: int = 0, salt: int = 0) -> np.ndarray:
     return _rng(ss).permutation(n).astype(np.int64)
 
 
+def router_weights(cfg: Config, seed: int = 0) -> np.ndarray:
+    """Router weights W_g [E][d] ~ N(0, 1/d) as bf16 bits, so x W_g^T has unit
+    scale for unit-scale x (inputs of the fused router front end)."""
+    return random_rows(cfg.E, cfg.d, "bf16", seed, salt=11, std=1.0 / np.sqrt(cfg.d))
+
+
 def random_rows(n_rows: int, d: int, dtype: str, seed: int = 0, salt: int = 0, std: float = 0.05):
     """Seeded random rows (e.g. stand-in expert outputs for combine-only cases)."""
     ss = _streams(seed)[_S_AUX].spawn(salt + 2)[salt + 1]
