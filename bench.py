@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--p", type=float, default=0.3, help="pruning threshold (paper: 0.3 for Qwen3)")
     ap.add_argument("--c", type=float, default=5.0, help="inter-node cost")
     ap.add_argument("--rank", type=int, default=0)
+    ap.add_argument("--eager", action="store_true",
+                    help="time eager launches (default: the step captured once as a HIP graph, replayed)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-stride", type=int, default=4, help="oracle FFN runs every n-th rank-0 row")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -337,6 +339,25 @@ def main():
     ms_per_step = t_start.elapsed_time(t_end) / K
     ffn_ms = sum(a.elapsed_time(b) for a, b in ffn_ev) / K
     log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
+    eager_ms_per_step = ms_per_step
+    graph_ms_per_step = None
+    if not args.eager:
+        # the same step captured once as a HIP graph and replayed K times
+        graph = L.capture_step(rank, side=side)
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        wall0 = time.perf_counter()
+        g0.record(stream)
+        for _ in range(K):
+            graph.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - wall0
+        graph_ms_per_step = g0.elapsed_time(g1) / K
+        ms_per_step = graph_ms_per_step
+        log(f"graph replays: {graph_ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step)")
 
     # per-stage breakdown (separate, untimed pass)
     stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
@@ -445,6 +466,7 @@ def main():
             "fused_router_front_end": front_end,
             "rank_rows": rows, "rank_received_tokens": U,
             "host_wall_ms_per_step": 1e3 * wall / K,
+            "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
         },
     }
     if not args.no_cpu:

@@ -209,6 +209,23 @@ class DeviceLayer:
         self.shared_ffn(rank, stream)
         self.src_reduce(rank, stream)
 
+    def capture_step(self, rank: int = 0, side=None, warmup: int = 2) -> torch.cuda.CUDAGraph:
+        """The whole step (front end, then rank `rank`'s path) as one HIP graph.
+        Every call writes fixed buffers and allocates nothing, so replays redo
+        exactly the eager work."""
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            for _ in range(warmup):
+                self.front(side=side)
+                self.rank_path(rank)
+        torch.cuda.current_stream().wait_stream(cap)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.front(side=side)
+            self.rank_path(rank)
+        return g
+
     def step(self, rank: int = 0, stream=None):
         self.front(stream)
         self.rank_path(rank, stream)

@@ -164,6 +164,38 @@ def test_router_route_odd_shapes(T, E, k, R, rpn, d, p):
     _check_router_route(L, cfg, x, wg, er)
 
 
+def test_graph_replay_matches_eager():
+    """The captured step, replayed three times with eager work and host syncs
+    in between, reproduces the eager step's outputs bit for bit each time."""
+    name, kind, p = "c4", "coact", 0.1
+    case = C.Case(name, gen.CONFIGS[name], kind, p)
+    cfg = case.cfg
+    er, el = C.placement(name, kind, p, 5.0)
+    L = _layer(case, x=gen.activations(cfg))
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    L.set_shared_weights(*gen.shared_weights(cfg))
+    g0 = torch.Generator(device="cuda").manual_seed(11)
+    L.parts.copy_((torch.randn(L.parts.shape, generator=g0, device="cuda") * 0.05).to(L.tdt))
+    side = torch.cuda.Stream()
+    L.front(side=side)
+    L.rank_path(0)
+    torch.cuda.synchronize()
+    names = ("y", "Y", "coact", "idx", "w", "mask", "row_src")
+    want = {n: L.host(n).copy() for n in names}
+    graph = L.capture_step(0, side=side)
+    for rep in range(3):
+        L.y.zero_()
+        L.Y.zero_()
+        L.coact.zero_()
+        L.idx.fill_(-1)
+        L.route()                                   # eager work between replays
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            assert np.array_equal(L.host(n).view(np.uint8), want[n].view(np.uint8)), (rep, n)
+
+
 def _adversarial_logits(T, E, seed):
     rng = np.random.default_rng(seed)
     L = rng.standard_normal((T, E)).astype(np.float32)
