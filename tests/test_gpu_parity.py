@@ -516,6 +516,50 @@ def test_layer_tiny_fp32_end_to_end(cfgname, kind, p):
         assert C.rel_fro(got, ref) <= 1e-5
 
 
+@pytest.mark.parametrize("fused", [False, True])
+def test_rank_with_no_rows(fused):
+    """A degenerate placement: one rank's experts are never selected, so it
+    computes no expert rows and receives no tokens.  Its permutation, FFN and
+    destination reduce are empty calls; every source rank's result still
+    equals the dense Eq. 1 path (c1u shape, fp32)."""
+    cfg = gen.CONFIGS["c1u"]
+    p = 0.3
+    er, el = gen.sequential_placement(cfg)
+    logits = gen.logits(cfg).copy()
+    idle = cfg.R - 1
+    logits[:, er == idle] -= 60.0                     # never in any token's top k
+    x = gen.activations(cfg)
+    L = DeviceLayer(cfg, logits, x, er, el, p, 5.0)
+    L.fused_gather = fused
+    for rank in range(cfg.R):
+        L.set_rank_weights(rank, *C.rank_weights(cfg, er, el, rank))
+    L.front()
+    torch.cuda.synchronize()
+    assert L.rank_rows(idle) == 0
+    rec = L.host("recv_offsets")
+    assert rec[idle + 1] == rec[idle]
+    for rank in range(cfg.R):
+        if fused:
+            L.row_source(rank)
+            L.ffn_gather(rank)
+        else:
+            L.gather(rank)
+            L.ffn(rank)
+        L.dest_reduce(rank)
+    r = oracle.route_prune(logits, cfg.k, er, cfg.ranks_per_node, cfg.tokens_per_rank, 5.0, p)
+    assert not np.isin(r["idx"], np.flatnonzero(er == idle)).any()
+    wts = {e: gen.expert_weights_f32(cfg, e) for e in range(cfg.E)}
+    for s in range(cfg.R):
+        L.src_reduce(s)
+        torch.cuda.synchronize()
+        toks = np.arange(s * cfg.tokens_per_rank, (s + 1) * cfg.tokens_per_rank)
+        ref = oracle.dense_moe_rows(toks, x[toks], r, lambda e: wts[e])
+        got = L.host("y")
+        ok, worst = C.within_tol(got, ref, atol=1e-5, rtol=1e-4)
+        assert ok, (s, worst)
+        assert C.rel_fro(got, ref) <= 1e-5
+
+
 def test_combine_bf16_full_size_sampled():
     """C2 coact p=0.3, rank 0: destination reduce of the real FFN output on
     sampled received tokens, and source reduce of seeded returned rows."""
