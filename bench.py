@@ -340,7 +340,7 @@ def main():
     ffn_ms = sum(a.elapsed_time(b) for a, b in ffn_ev) / K
     log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
     eager_ms_per_step = ms_per_step
-    graph_ms_per_step = None
+    graph_ms_per_step = cold_ms_per_step = None
     if not args.eager:
         # the same step captured once as a HIP graph and replayed K times
         graph = L.capture_step(rank, side=side)
@@ -358,6 +358,21 @@ def main():
         graph_ms_per_step = g0.elapsed_time(g1) / K
         ms_per_step = graph_ms_per_step
         log(f"graph replays: {graph_ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step)")
+        # the same replays with the caches cold: 512 MB (twice the 256 MB
+        # Infinity Cache) rewritten before each, outside its timed window
+        flush = torch.zeros(512 << 20, dtype=torch.uint8, device="cuda")
+        cold = []
+        for _ in range(min(K, 10)):
+            flush.add_(1)
+            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            c0.record(stream)
+            graph.replay()
+            c1.record(stream)
+            torch.cuda.synchronize()
+            cold.append(c0.elapsed_time(c1))
+        cold_ms_per_step = float(np.median(cold))
+        del flush
+        log(f"cold-cache replays: {cold_ms_per_step:.4f} ms/step (median of {len(cold)})")
 
     # per-stage breakdown (separate, untimed pass)
     stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
@@ -467,6 +482,7 @@ def main():
             "rank_rows": rows, "rank_received_tokens": U,
             "host_wall_ms_per_step": 1e3 * wall / K,
             "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
+            "cold_cache_ms_per_step": cold_ms_per_step,
         },
     }
     if not args.no_cpu:
