@@ -262,7 +262,14 @@ cap_status cap_permute(const cap_topology *topo, cap_permute_mode mode, int32_t 
  *       needs d % 256 == 0 and inter % 128 == 0.
  * f32:  fp32 throughout; needs d % 4 == 0.
  * Shared experts: call with E_loc = 1, row_offsets = {0, n}, inter = the
- * concatenated intermediate size.  Workspace: cap_workspace_size(CAP_OP_EXPERT_FFN).
+ * concatenated intermediate size.  Workspace: cap_workspace_size(CAP_OP_EXPERT_FFN):
+ * H [max_rows][inter] and, for bf16, the counters of the fused kernel; its
+ * contents need no initialisation.
+ * bf16 calls with max_rows >= 8192 run both GEMMs in one kernel with a tile
+ * queue per XCD (a down tile starts once the gate/up tiles of its rows are
+ * done); smaller calls run one kernel per GEMM.  Both give the same bits.
+ * The environment variable CAP_FFN_FUSED_GRID=n caps the fused kernel's grid
+ * at n workgroups (for tests; the result does not change).
  */
 cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter,
                           int32_t max_rows, const void *xs, const int32_t *row_offsets,

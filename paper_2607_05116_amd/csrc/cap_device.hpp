@@ -52,8 +52,9 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
     return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
-// Grid-wide launch helper: number of blocks for a persistent grid.
+// Grid-wide launch helpers: compute units and XCDs of the current device.
 int device_cu_count();
+int device_xcc_count();
 
 }  // namespace cap
 

@@ -41,6 +41,19 @@ int device_cu_count() {
     return n;
 }
 
+// XCD (XCC) count of the current device, cached per device.
+int device_xcc_count() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v > 0) return v;
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || n <= 0) n = 1;
+    cache[dev].store(n, std::memory_order_relaxed);
+    return n;
+}
+
 namespace {
 
 bool topo_ok(const cap_topology* t) {

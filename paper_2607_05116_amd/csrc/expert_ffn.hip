@@ -1,8 +1,8 @@
 // Grouped SwiGLU expert FFN over one rank's experts (Eq. 1, Expert_i(x); the
 // experts are SwiGLU FFNs: y = W2 (silu(W1 x) * (W3 x))).
 //
-// Two grouped GEMMs per call, each a persistent kernel with a device-side tile
-// scheduler over the ragged experts (row offsets are read on the device):
+// Two grouped GEMMs per call over the ragged experts (row offsets are read on
+// the device):
 //   gate/up   H[m][j] = silu(X W1^T)[m][j] * (X W3^T)[m][j]   (K = d)
 //   down      Y[m][o] = (H W2^T)[m][o]                         (K = inter)
 //
@@ -16,19 +16,14 @@
 //   * Half of the waves issue all the stage loads and the other half all the
 //     output stores, so no wave's in-order memory counter mixes the two (a
 //     wait for a stage never waits for a tile's worth of stores to drain).
-//   * The MFMA is issued with the weight fragment as its first operand, so a
-//     lane's 16 accumulators hold 4 consecutive output columns per register
-//     group; lanes r and r + 32 exchange halves so each stores 16 bytes.
-//   * Gate/up: the B tile interleaves 32-row blocks of W1 and W3 (W1 rows j..j+31,
-//     then W3 rows j..j+31, ...), so the gate and up accumulators of one output
-//     element sit in the same lane and register; SiLU-and-multiply happens in
-//     registers and H is rounded to bf16 once.
-//   * Tiles are ordered expert, m-tile, n-tile (n fastest: neighbours share the
-//     X rows); block b runs on XCD b % 8, so the block -> worker map gives each
-//     XCD a contiguous run of tiles and their operands share that XCD's L2.
+//   * Calls of many m-tiles run both GEMMs in one persistent kernel with a
+//     tile queue per XCD (ffn_fused_bf16_kernel); calls of few m-tiles run one
+//     persistent kernel per GEMM (ffn_gemm_bf16_kernel).  Every output element
+//     takes the same arithmetic in both, so the two give identical bits.
 // fp32 path: a plain LDS-tiled FMA kernel (small shapes only).
 #include "cap_device.hpp"
 
+#include <cstdlib>
 #include <type_traits>
 
 namespace cap {
@@ -46,11 +41,6 @@ __device__ __forceinline__ void static_for(F&& f) {
 }
 
 // ------------------------------------------------------------------ tile scheduler
-struct Sched {
-    int n_tiles;        // tiles along N
-    int total;          // total tiles
-};
-
 // Fills mt_prefix[0..E_loc] (m-tiles before each expert) and row bounds.
 template <int BM>
 __device__ void build_schedule(const int32_t* row_offsets, int E_loc, int max_rows, int* mt_prefix,
@@ -208,285 +198,575 @@ __device__ __forceinline__ void wait_vmem(int n) {
 typedef __attribute__((address_space(3))) void lds_void;
 
 
-// Roles.  Loads and stores share one in-order completion counter per wave,
-// so a wave that stores its outputs and then waits for a stage would also
-// wait for every store to drain (a whole tile of outputs per CU, all CUs at
-// once).  The first half of the waves ("loaders") therefore issue every
-// direct-to-LDS stage load and never store to global memory: they leave their
-// outputs in an LDS staging area.  The other half ("storers") issue no loads;
-// they write their own outputs and the staged ones, and never wait for
+// ------------------------------------------------------------------ shared tile pieces
+// Block tile 256 x 256, eight waves in a 4 x 2 grid, each wave 64 x 128.
+constexpr int kBM = 256, kBN = 256, kWavesM = 4, kWavesN = 2;
+constexpr int kNW = kWavesM * kWavesN;
+constexpr int kNL = kNW / 2;                          // loader waves; the rest are storers
+constexpr int kWM = kBM / kWavesM, kWN = kBN / kWavesN;
+constexpr int kMI = kWM / 32, kNJ = kWN / 32;         // 32 x 32 MFMA blocks per wave
+constexpr int kRowsPerLoad = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
+constexpr int kALd = kBM / kRowsPerLoad / kNL;        // direct loads per loader wave per stage
+constexpr int kBLd = kBN / kRowsPerLoad / kNL;
+constexpr int kBRun = kBLd / 2;                       // a loader's B rows: two runs of 32
+constexpr int kStageBytes = (kBM + kBN) * kRowB;
+static_assert(kNL % 4 == 0, "one loader and one storer wave per SIMD");
+static_assert(kBM % (kRowsPerLoad * kNL) == 0 && kBN % (kRowsPerLoad * kNL) == 0, "load split");
+static_assert(kALd + kBLd <= 60, "loads per stage must fit the vmcnt field");
+static_assert(kWN % 64 == 0, "gate/up pairs need 64-column wave tiles");
+static_assert(kBRun * kRowsPerLoad == 32, "a gate/up loader covers one 32-row W1/W3 pair");
+static_assert(kStageK % 32 == 0, "fragments are read two K steps at a time");
+static_assert(kStages == 2, "staging lives in stage buffer 1");
+
+// One stage of a wave's MFMA work: its 64 x 128 block over the stage's K = 64,
+// fragments read from LDS two K steps at a time.  The MFMA takes the weight
+// fragment as its first operand, so a lane's 16 accumulators hold 4
+// consecutive output columns per register group.
+__device__ __forceinline__ void mma_stage(const uint8_t* sa, const uint8_t* sb, int wm, int wn, int fr_row,
+                                          int fr_swz, int fr_half, f32x16 (&acc)[kMI][kNJ]) {
+    constexpr int KS = kStageK / 16;                  // MFMA K steps per stage
+#pragma unroll
+    for (int k2 = 0; k2 < KS; k2 += 2) {
+        bf16x8 fa[2][kMI], fb[2][kNJ];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int pc = ((2 * (k2 + ks) + fr_half) ^ fr_swz) << 4;
+#pragma unroll
+            for (int i = 0; i < kMI; ++i)
+                fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * kWM + i * 32 + fr_row) * kRowB + pc);
+#pragma unroll
+            for (int j = 0; j < kNJ; ++j)
+                fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * kWN + j * 32 + fr_row) * kRowB + pc);
+        }
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int i = 0; i < kMI; ++i)
+#pragma unroll
+                for (int j = 0; j < kNJ; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMI + kNJ), 0);   // DS reads
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * kMI * kNJ, 0);     // MFMA
+    }
+}
+
+// Epilogue of a tile of rows [row0, row0 + rows) and block column nt.
+// Lane (r, h) = (lane % 32, lane / 32) holds, for register group g, columns
+// 8g + 4h + 0..3 of row r of each 32 x 32 block.  Lanes r and r + 32 swap
+// halves (permlane32_swap) so that each holds 8 consecutive columns: groups
+// (0, 1) -> lane r columns 0..7, lane r + 32 columns 8..15; groups (2, 3)
+// likewise at 16 and 24.  Gate/up: the B tile interleaves 32-row blocks of W1
+// and W3, so acc[i][2b] and acc[i][2b + 1] are the gate and up sums of the
+// same outputs; SiLU-and-multiply happens in registers and H is rounded to
+// bf16 once.  Loader waves write their 16-byte pieces to the staging area
+// (stage buffer 1), storer waves to the output; after a barrier the storers
+// also write the staged rows.  Storers never wait for their stores here.
+template <bool GUP>
+__device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16_t* __restrict__ out, int N_out,
+                                           int row0, int rows, int nt, int wave, int lane, uint8_t* staging) {
+    constexpr int OUT_C = GUP ? kWN / 2 : kWN;        // output columns of a wave tile
+    constexpr int OUT_RB = OUT_C * 2;                 // bytes per staged output row
+    constexpr int OUT_CH = OUT_RB / 16;               // 16-byte chunks per staged row
+    constexpr int OUT_RPW = 256 / OUT_RB;             // staged rows per 256-byte bank window
+    constexpr int STG_B = kWM * OUT_RB;               // staging bytes per loader wave
+    constexpr int NB = GUP ? kNJ / 2 : kNJ;           // 32-column output blocks of a wave
+    static_assert(kNL * STG_B <= kStageBytes, "staging fits in stage buffer 1");
+    static_assert(OUT_RB == 128 || OUT_RB == 256, "staged row layout");
+    // staged output rows: 16-byte chunk c of row r at physical chunk
+    // c ^ ((r / OUT_RPW) % OUT_CH), conflict-free for column writes and row reads
+    auto stg_swz = [](int r) { return (r / OUT_RPW) & (OUT_CH - 1); };
+    const bool loader = wave < kNL;
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
+    // the lane index is made opaque so that lane-derived addresses are formed
+    // here, per tile, and not kept live across the K loop
+    int ep_lane = lane;
+    asm volatile("" : "+v"(ep_lane));
+    const int ep_row = ep_lane & 31, ep_half = ep_lane >> 5;
+    uint8_t* my_stg = staging + (loader ? wave : 0) * STG_B;
+    const int out_c0 = (GUP ? nt * (kBN / 2) : nt * kBN) + wn * OUT_C;
+#pragma unroll
+    for (int i = 0; i < kMI; ++i) {
+        if (!loader && wm * kWM + i * 32 >= rows) continue;            // wave-uniform
+        const int r = i * 32 + ep_row;                                 // row within the wave tile
+        const bool row_ok = wm * kWM + r < rows;
+        uint16_t* crow = out + static_cast<size_t>(row0 + wm * kWM + r) * N_out + out_c0;
+#pragma unroll
+        for (int jb = 0; jb < NB; ++jb) {
+            float v[16];
+            if constexpr (GUP) {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) v[e] = silu(acc[i][2 * jb][e]) * acc[i][2 * jb + 1][e];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 16; ++e) v[e] = acc[i][jb][e];
+            }
+#pragma unroll
+            for (int gp = 0; gp < 4; gp += 2) {
+                const uint32_t x0 = pack_bf16x2_rne(v[4 * gp + 0], v[4 * gp + 1]);
+                const uint32_t x1 = pack_bf16x2_rne(v[4 * gp + 2], v[4 * gp + 3]);
+                const uint32_t y0 = pack_bf16x2_rne(v[4 * gp + 4], v[4 * gp + 5]);
+                const uint32_t y1 = pack_bf16x2_rne(v[4 * gp + 6], v[4 * gp + 7]);
+                const auto ra = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+                const auto rb = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+                u32x4 o;
+                o[0] = ra[0]; o[1] = rb[0]; o[2] = ra[1]; o[3] = rb[1];
+                const int c = jb * 4 + gp + ep_half;                   // 8-column chunk in the wave tile
+                if (loader) {
+                    *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = o;
+                } else if (row_ok) {
+                    *reinterpret_cast<u32x4*>(crow + 8 * c) = o;
+                }
+            }
+        }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    block_barrier();                                                   // staging written
+    if (!loader) {
+        // storer wave w writes the staged tile of loader wave w - kNL
+        const int lw = wave - kNL;
+        const int lwm = lw / kWavesN, lwn = lw % kWavesN;
+        const uint8_t* stg = staging + lw * STG_B;
+        const int l_c0 = (GUP ? nt * (kBN / 2) : nt * kBN) + lwn * OUT_C;
+        constexpr int ROWS_PER_READ = 1024 / OUT_RB;
+#pragma unroll
+        for (int r0 = 0; r0 < kWM; r0 += ROWS_PER_READ) {
+            if (lwm * kWM + r0 >= rows) break;                          // wave-uniform
+            const int r = r0 + ep_lane / OUT_CH;
+            const int c = ep_lane % OUT_CH;
+            const u32x4 vv = *reinterpret_cast<const u32x4*>(stg + r * OUT_RB + 16 * (c ^ stg_swz(r)));
+            if (lwm * kWM + r < rows)
+                *reinterpret_cast<u32x4*>(out + static_cast<size_t>(row0 + lwm * kWM + r) * N_out + l_c0 + 8 * c) = vv;
+        }
+    }
+}
+
+// Per-lane constants of the direct loads and the fragment reads.
+struct LaneMap {
+    int ld_row;          // direct loads: lane l writes row l / 8 of its 1 KiB block ...
+    uint32_t col_b[2];   // ... at physical chunk l % 8, fetching logical chunk (l % 8) ^ swz(row):
+                         // the swizzle of row (8 * blk + l / 8) is swz(l / 8) ^ (blk & 1)
+    int fr_row, fr_swz, fr_half;   // fragment reads: row r = ... + lane % 32, K half lane / 32
+};
+__device__ __forceinline__ LaneMap lane_map(int lane) {
+    LaneMap m;
+    m.ld_row = lane >> 3;
+    const int pc = lane & (kChunks - 1);
+    m.col_b[0] = static_cast<uint32_t>((pc ^ lds_swz(m.ld_row)) * 16);
+    m.col_b[1] = static_cast<uint32_t>((pc ^ lds_swz(kRowsPerLoad + m.ld_row)) * 16);
+    m.fr_row = lane & 31;
+    m.fr_swz = lds_swz(m.fr_row);
+    m.fr_half = lane >> 5;
+    return m;
+}
+
+// Operand sources of one tile for one loader wave: A rows (or, gathered, the
+// base of x) and the wave's two 32-row B runs; pitch = bytes per operand row.
+struct TileSrc {
+    const char* a;
+    const char* b[2];
+    uint32_t pitch, blk;                 // row pitch; bytes per 8-row block
+    int rows;                            // valid A rows (past them: the last row again)
+};
+
+// Issues one stage's direct-to-LDS loads of a loader wave into stage buffer
+// kt % 2: A rows wave * 64 .. + 63 and the wave's 64 B rows.  a_off holds the
+// per-lane byte offsets of gathered A rows (gathered = true).
+__device__ __forceinline__ void issue_stage(const TileSrc& s, int kt, int wave, const LaneMap& lm,
+                                            const uint32_t (&lane_off)[2], bool gathered,
+                                            const uint32_t* a_off, uint32_t lds_base) {
+    const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * kStageBytes);
+    const uint32_t kb = static_cast<uint32_t>(kt) * kStageK * 2;
+    const uint32_t a_lds = st + wave * kALd * 1024;
+    const int a_first = wave * kALd * kRowsPerLoad;
+    if (gathered) {
+        static_for<kALd>([&](auto I) { lds_dma16_at(s.a, a_off[I.value], kb, a_lds + I.value * 1024); });
+    } else if (a_first + kALd * kRowsPerLoad <= s.rows) {                 // wave-uniform
+        const char* a_base = s.a + kb + static_cast<size_t>(wave * kALd) * s.blk;
+        static_for<kALd>([&](auto I) {
+            lds_dma16_blk<I.value>(a_base, lane_off[(wave * kALd + I.value) & 1], s.blk, a_lds + I.value * 1024);
+        });
+    } else {
+        // the last tile of an expert: rows past its end repeat its last row
+        static_for<kALd>([&](auto I) {
+            lds_dma16_clamped(s.a + kb, lm.ld_row, a_first + I.value * kRowsPerLoad, s.rows - 1, s.pitch,
+                              lm.col_b[(wave * kALd + I.value) & 1], a_lds + I.value * 1024);
+        });
+    }
+    const uint32_t b_lds = st + kBM * kRowB + wave * kBLd * 1024;
+    static_for<kBLd>([&](auto I) {
+        constexpr int i = decltype(I)::value;
+        lds_dma16_blk<i % kBRun>(s.b[i / kBRun] + kb, lane_off[(wave * kBLd + i) & 1], s.blk, b_lds + i * 1024);
+    });
+}
+
+// Sources of tile (expert l, rows [row0, row0 + rows), block column nt) for
+// loader wave lw.  Gate/up: A = x (K = d), B runs = W1 and W3 rows
+// nt * 128 + lw * 32 .. + 31 (the B tile interleaves 32-row blocks of W1 and
+// W3); down: A = H (K = inter), B runs = W2 rows nt * 256 + lw * 64 .. + 63.
+__device__ __forceinline__ TileSrc tile_src(bool gu, bool gathered, const uint16_t* A, const uint16_t* B0,
+                                            const uint16_t* B1, int l, int row0, int rows, int nt, int lw, int K,
+                                            int N_out) {
+    TileSrc s;
+    s.pitch = static_cast<uint32_t>(K) * 2u;
+    s.blk = static_cast<uint32_t>(kRowsPerLoad) * s.pitch;
+    s.rows = rows;
+    s.a = gathered ? reinterpret_cast<const char*>(A) : reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
+    if (gu) {
+        const size_t row = static_cast<size_t>(l) * N_out + nt * (kBN / 2) + lw * 32;
+        s.b[0] = reinterpret_cast<const char*>(B0 + row * K);
+        s.b[1] = reinterpret_cast<const char*>(B1 + row * K);
+    } else {
+        const size_t row = static_cast<size_t>(l) * N_out + nt * kBN + lw * kBLd * kRowsPerLoad;
+        s.b[0] = reinterpret_cast<const char*>(B0 + row * K);
+        s.b[1] = reinterpret_cast<const char*>(B0 + (row + 32) * K);
+    }
+    return s;
+}
+
+// Lane byte offsets of the current tile's loads (pitch-dependent) and, for
+// gathered A, of each A row this lane loads (x row row_src[row0 + r],
+// clamped into [0, x_rows)).
+__device__ __forceinline__ void lane_offsets(const TileSrc& s, const LaneMap& lm, uint32_t (&lane_off)[2]) {
+    lane_off[0] = lm.ld_row * s.pitch + lm.col_b[0];
+    lane_off[1] = lm.ld_row * s.pitch + lm.col_b[1];
+}
+__device__ __forceinline__ void gather_offsets(const TileSrc& s, const LaneMap& lm, int wave, int row0,
+                                               const int32_t* __restrict__ row_src, int x_rows,
+                                               uint32_t (&a_off)[kALd]) {
+#pragma unroll
+    for (int i = 0; i < kALd; ++i) {
+        const int r = min(wave * kALd * kRowsPerLoad + i * kRowsPerLoad + lm.ld_row, s.rows - 1);
+        int tok = row_src[row0 + r];
+        tok = min(max(tok, 0), x_rows - 1);
+        a_off[i] = static_cast<uint32_t>(tok) * s.pitch + lm.col_b[(wave * kALd + i) & 1];
+    }
+}
+
+// ------------------------------------------------------------------ two-kernel bf16 path
+// One persistent kernel per GEMM (used for calls of few m-tiles).  Roles:
+// loads and stores share one in-order completion counter per wave, so a wave
+// that stores its outputs and then waits for a stage would also wait for
+// every store to drain (a whole tile of outputs per CU, all CUs at once).  The
+// loader waves therefore issue every direct-to-LDS stage load and never store
+// to global memory (they stage their outputs in LDS); the storer waves issue
+// no loads, write their own and the staged outputs, and never wait for
 // stores.  The staging area is stage buffer 1, free from the end of a tile's K
 // loop until the next tile fills its stage 1 (one barrier later).
-//
-// GATHER: row i of A is A[row_src[i]] (A has x_rows rows): each loader lane
-// keeps the byte offsets of the rows it loads for the current tile.
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool GATEUP, bool GATHER>
-__global__ __launch_bounds__(WAVES_M * WAVES_N * kWave, 1) void ffn_gemm_bf16_kernel(
+// Tiles are ordered expert, m-tile, n-tile (n fastest: neighbours share the A
+// rows); block b runs on XCD b % 8, so the block -> worker map gives each XCD
+// a contiguous run of tiles and their operands share that XCD's L2.
+// GATHER: row i of A is A[row_src[i]] (A has x_rows rows).
+template <bool GATEUP, bool GATHER>
+__global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
     uint16_t* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K,
     int N_out, const int32_t* __restrict__ row_src, int x_rows) {
-    constexpr int NW = WAVES_M * WAVES_N;
-    constexpr int NL = NW / 2;                             // loader waves
-    constexpr int WM = BM / WAVES_M, WN = BN / WAVES_N;
-    constexpr int MI = WM / 32, NJ = WN / 32;
-    constexpr int KS = kStageK / 16;                       // MFMA K steps per stage
-    constexpr int ROWS_PER_LOAD = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
-    constexpr int A_LD = BM / ROWS_PER_LOAD / NL;          // direct loads per loader wave per stage
-    constexpr int B_LD = BN / ROWS_PER_LOAD / NL;
-    constexpr int STAGE_B = (BM + BN) * kRowB;
-    constexpr int OUT_C = GATEUP ? WN / 2 : WN;            // output columns of a wave tile
-    constexpr int OUT_RB = OUT_C * 2;                      // bytes per staged output row
-    constexpr int OUT_CH = OUT_RB / 16;                    // 16-byte chunks per staged row
-    constexpr int OUT_RPW = 256 / OUT_RB;                  // staged rows per 256-byte bank window
-    constexpr int STG_B = WM * OUT_RB;                     // staging bytes per loader wave
-    static_assert(NW % 2 == 0 && NL % 4 == 0, "one loader and one storer wave per SIMD");
-    static_assert(BM % (ROWS_PER_LOAD * NL) == 0 && BN % (ROWS_PER_LOAD * NL) == 0, "load split");
-    static_assert(A_LD + B_LD <= 60, "loads per stage must fit the vmcnt field");
-    static_assert(!GATEUP || (WN % 64 == 0), "gate/up pairs need 64-column wave tiles");
-    static_assert(32 % ROWS_PER_LOAD == 0, "a direct load must stay inside one W1/W3 block");
-    static_assert(KS % 2 == 0, "fragments are read two K steps at a time");
-    static_assert(kStages == 2 && NL * STG_B <= STAGE_B, "staging lives in stage buffer 1");
-    static_assert(OUT_RB == 128 || OUT_RB == 256, "staged row layout");
-
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * STAGE_B];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
     __shared__ int row_begin[kMaxExpertsLocal];
     __shared__ int row_end[kMaxExpertsLocal];
 
-    build_schedule<BM>(row_offsets, E_loc, max_rows, mt_prefix, row_begin, row_end);
-    const int n_tiles = GATEUP ? N_out / (BN / 2) : N_out / BN;
+    build_schedule<kBM>(row_offsets, E_loc, max_rows, mt_prefix, row_begin, row_end);
+    const int n_tiles = GATEUP ? N_out / (kBN / 2) : N_out / kBN;
     const int total = mt_prefix[E_loc] * n_tiles;
     const int KT = K / kStageK;
     const int lane = threadIdx.x % kWave;
-    const uint32_t wave_u = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-    const int wave = static_cast<int>(wave_u);
-    const bool loader = wave < NL;
-    const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+    const int wave = static_cast<int>(__builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
+    const bool loader = wave < kNL;
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
-    uint8_t* const staging = lds + STAGE_B;                // stage buffer 1
+    const LaneMap lm = lane_map(lane);
 
-    // direct-load lane mapping: lane l writes row (l >> 3) of its 1 KiB block
-    // at physical chunk (l & 7), so it fetches logical chunk (l & 7) ^ swz(row)
-    // (the swizzle of a tile row depends on the block parity too).
-    const int ld_row = lane >> 3;
-    const int ld_pc = lane & (kChunks - 1);
-    // fragment lane mapping (row r = ... + (lane & 31); swz depends on lane & 31 only)
-    const int fr_row = lane & 31;
-    const int fr_swz = lds_swz(fr_row);
-    const int fr_half = lane >> 5;
-    // staged output rows: 16-byte chunk c of row r at physical chunk
-    // c ^ ((r / OUT_RPW) % OUT_CH), conflict-free for column writes and row reads
-    auto stg_swz = [&](int r) { return (r / OUT_RPW) & (OUT_CH - 1); };
-
-    // Per-tile load sources (loader waves): wave-uniform byte bases.  A rows
-    // past the expert's end are clamped to its last row (never stored).
-    // A loader's B rows are one contiguous run (down) or two (gate/up: its
-    // W1 rows, then the matching W3 rows), so two scalar bases cover them.
-    constexpr int B_RUN = GATEUP ? B_LD / 2 : B_LD;        // loads per contiguous B run
-    static_assert(!GATEUP || B_RUN * ROWS_PER_LOAD == 32, "a gate/up loader covers one 32-row W1/W3 pair");
-    struct TileSrc {
-        const char* a;              // A + row0 * K (GATHER: A)
-        int a_last;                 // last valid row of the tile
-        const char* b[2];           // first row of each B run
-    };
-    auto tile_sources = [&](int tile, int& row0, int& rows_valid, int& nt) {
-        TileSrc src;
+    int row0 = 0, rows = 0, nt = 0;
+    TileSrc src;
+    uint32_t lane_off[2] = {0, 0};
+    uint32_t a_off[kALd];
+    auto start_tile = [&](int tile) {
         const int m_tile = tile / n_tiles;
         nt = tile % n_tiles;
         // wave-uniform: keep them in scalar registers
         const int l = __builtin_amdgcn_readfirstlane(find_expert(mt_prefix, E_loc, m_tile));
-        row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (m_tile - mt_prefix[l]) * BM);
-        rows_valid = __builtin_amdgcn_readfirstlane(min(BM, row_end[l] - row0));
-        src.a = GATHER ? reinterpret_cast<const char*>(A)
-                       : reinterpret_cast<const char*>(A + static_cast<size_t>(row0) * K);
-        src.a_last = rows_valid - 1;
-        const int lw = loader ? wave : 0;
-        if constexpr (GATEUP) {
-            const size_t row = static_cast<size_t>(l) * N_out + nt * (BN / 2) + lw * 32;
-            src.b[0] = reinterpret_cast<const char*>(B0 + row * K);
-            src.b[1] = reinterpret_cast<const char*>(B1 + row * K);
-        } else {
-            const size_t row = static_cast<size_t>(l) * N_out + nt * BN + lw * B_LD * ROWS_PER_LOAD;
-            src.b[0] = src.b[1] = reinterpret_cast<const char*>(B0 + row * K);
-        }
-        return src;
-    };
-    // Lane byte offsets of a direct load within its 8-row block: the swizzle
-    // of row (blk * 8 + ld_row) is ld_row ^ (blk & 1), so two values cover
-    // every block; the block's own row offset is added inside the load.
-    const uint32_t col_b[2] = {static_cast<uint32_t>((ld_pc ^ lds_swz(ld_row)) * 16),
-                               static_cast<uint32_t>((ld_pc ^ lds_swz(ROWS_PER_LOAD + ld_row)) * 16)};
-    const uint32_t pitch = static_cast<uint32_t>(K) * 2u;                 // bytes per operand row
-    const uint32_t lane_off[2] = {ld_row * pitch + col_b[0], ld_row * pitch + col_b[1]};
-    const uint32_t blk_bytes = static_cast<uint32_t>(ROWS_PER_LOAD) * pitch;
-    // GATHER: byte offset (row and chunk) of each A row this loader lane loads
-    uint32_t a_off[GATHER ? A_LD : 1];
-    auto gather_offsets = [&](int tile_row0, int a_last) {
-        if constexpr (GATHER) {
-            if (!loader) return;
-#pragma unroll
-            for (int i = 0; i < A_LD; ++i) {
-                const int r = min(wave * A_LD * ROWS_PER_LOAD + i * ROWS_PER_LOAD + ld_row, a_last);
-                int tok = row_src[tile_row0 + r];
-                tok = min(max(tok, 0), x_rows - 1);
-                a_off[i] = static_cast<uint32_t>(tok) * pitch + col_b[(wave * A_LD + i) & 1];
-            }
-        }
-    };
-    auto issue_stage = [&](const TileSrc& src, int kt) {
+        row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (m_tile - mt_prefix[l]) * kBM);
+        rows = __builtin_amdgcn_readfirstlane(min(kBM, row_end[l] - row0));
         if (!loader) return;
-        const uint32_t st = lds_base + static_cast<uint32_t>((kt % kStages) * STAGE_B);
-        const size_t kb = static_cast<size_t>(kt) * kStageK * 2;
-        const char* a_base = src.a + kb + static_cast<size_t>(wave * A_LD) * blk_bytes;
-        const uint32_t a_lds = st + wave * A_LD * 1024;
-        const int a_first = wave * A_LD * ROWS_PER_LOAD;
-        if constexpr (GATHER) {
-            static_for<A_LD>([&](auto I) {
-                lds_dma16_at(src.a, a_off[I.value], static_cast<uint32_t>(kb), a_lds + I.value * 1024);
-            });
-        } else if (a_first + A_LD * ROWS_PER_LOAD - 1 <= src.a_last) {           // wave-uniform
-            static_for<A_LD>([&](auto I) {
-                lds_dma16_blk<I.value>(a_base, lane_off[(wave * A_LD + I.value) & 1], blk_bytes, a_lds + I.value * 1024);
-            });
-        } else {
-            // the last tile of an expert: rows past its end repeat its last row
-            static_for<A_LD>([&](auto I) {
-                lds_dma16_clamped(src.a + kb, ld_row, a_first + I.value * ROWS_PER_LOAD, src.a_last, pitch,
-                                  col_b[(wave * A_LD + I.value) & 1], a_lds + I.value * 1024);
-            });
-        }
-        const uint32_t b_lds = st + BM * kRowB + wave * B_LD * 1024;
-        static_for<B_LD>([&](auto I) {
-            constexpr int i = decltype(I)::value;
-            lds_dma16_blk<i % B_RUN>(src.b[i / B_RUN] + kb, lane_off[(wave * B_LD + i) & 1], blk_bytes,
-                                     b_lds + i * 1024);
-        });
+        src = tile_src(GATEUP, GATHER, A, B0, B1, l, row0, rows, nt, wave, K, N_out);
+        lane_offsets(src, lm, lane_off);
+        if constexpr (GATHER) gather_offsets(src, lm, wave, row0, row_src, x_rows, a_off);
+        issue_stage(src, 0, wave, lm, lane_off, GATHER, a_off, lds_base);
     };
 
     int tile = worker_id();
-    int row0 = 0, rows_valid = 0, nt = 0;
-    TileSrc src;
-    if (tile < total) {
-        src = tile_sources(tile, row0, rows_valid, nt);
-        gather_offsets(row0, src.a_last);
-        issue_stage(src, 0);
-    }
+    if (tile < total) start_tile(tile);
     while (tile < total) {
-        f32x16 acc[MI][NJ];
+        f32x16 acc[kMI][kNJ];
 #pragma unroll
-        for (int i = 0; i < MI; ++i)
+        for (int i = 0; i < kMI; ++i)
 #pragma unroll
-            for (int j = 0; j < NJ; ++j)
+            for (int j = 0; j < kNJ; ++j)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
         for (int kt = 0; kt < KT; ++kt) {
             if (loader) wait_vmem(0);              // this wave's part of stage kt has landed
             block_barrier();                       // stage kt visible; the other buffer is free
-            if (kt + 1 < KT) issue_stage(src, kt + 1);
-            const uint8_t* sa = lds + (kt % kStages) * STAGE_B;
-            const uint8_t* sb = sa + BM * kRowB;
-#pragma unroll
-            for (int k2 = 0; k2 < KS; k2 += 2) {
-                bf16x8 fa[2][MI], fb[2][NJ];
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const int pc = ((2 * (k2 + ks) + fr_half) ^ fr_swz) << 4;
-#pragma unroll
-                    for (int i = 0; i < MI; ++i)
-                        fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * WM + i * 32 + fr_row) * kRowB + pc);
-#pragma unroll
-                    for (int j = 0; j < NJ; ++j)
-                        fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * WN + j * 32 + fr_row) * kRowB + pc);
-                }
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-                    for (int i = 0; i < MI; ++i)
-#pragma unroll
-                        for (int j = 0; j < NJ; ++j)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
-                __builtin_amdgcn_sched_group_barrier(0x100, 2 * (MI + NJ), 0);   // DS reads
-                __builtin_amdgcn_sched_group_barrier(0x008, 2 * MI * NJ, 0);     // MFMA
-            }
+            if (loader && kt + 1 < KT) issue_stage(src, kt + 1, wave, lm, lane_off, GATHER, a_off, lds_base);
+            const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
+            mma_stage(sa, sa + kBM * kRowB, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, acc);
         }
 
         // every wave is done with this tile's LDS: loaders start the next
         // tile's stage 0 (buffer 0), buffer 1 becomes the staging area
         block_barrier();
-        const int cur_row0 = row0, cur_rows = rows_valid, cur_nt = nt;
+        const int cur_row0 = row0, cur_rows = rows, cur_nt = nt;
         const int next = tile + gridDim.x;
-        if (next < total) {
-            src = tile_sources(next, row0, rows_valid, nt);
-            gather_offsets(row0, src.a_last);
-            issue_stage(src, 0);
-        }
-
-        // Epilogue.  Lane (r, h) = (lane % 32, lane / 32) holds, for register
-        // group g, columns 8g + 4h + 0..3 of row r of each 32x32 block.  Lanes
-        // r and r + 32 swap halves (permlane32_swap) so that each holds 8
-        // consecutive columns: groups (0, 1) -> lane r columns 0..7, lane r + 32
-        // columns 8..15; groups (2, 3) likewise at 16 and 24.  Loaders write
-        // those 16 bytes to staging, storers to the output.
-        uint8_t* my_stg = staging + (loader ? wave : 0) * STG_B;
-        const int out_c0 = GATEUP ? cur_nt * (BN / 2) + wn * (WN / 2) : cur_nt * BN + wn * WN;
-#pragma unroll
-        for (int i = 0; i < MI; ++i) {
-            if (!loader && wm * WM + i * 32 >= cur_rows) continue;      // wave-uniform
-            const int r = i * 32 + fr_row;                              // row within the wave tile
-            const bool row_ok = wm * WM + r < cur_rows;
-            uint16_t* crow = C + static_cast<size_t>(cur_row0 + wm * WM + r) * N_out + out_c0;
-            constexpr int NB = GATEUP ? NJ / 2 : NJ;                    // 32-column output blocks
-#pragma unroll
-            for (int jb = 0; jb < NB; ++jb) {
-                float v[16];
-                if constexpr (GATEUP) {
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) v[e] = silu(acc[i][2 * jb][e]) * acc[i][2 * jb + 1][e];
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) v[e] = acc[i][jb][e];
-                }
-#pragma unroll
-                for (int gp = 0; gp < 4; gp += 2) {
-                    const uint32_t x0 = pack_bf16x2_rne(v[4 * gp + 0], v[4 * gp + 1]);
-                    const uint32_t x1 = pack_bf16x2_rne(v[4 * gp + 2], v[4 * gp + 3]);
-                    const uint32_t y0 = pack_bf16x2_rne(v[4 * gp + 4], v[4 * gp + 5]);
-                    const uint32_t y1 = pack_bf16x2_rne(v[4 * gp + 6], v[4 * gp + 7]);
-                    const auto ra = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-                    const auto rb = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-                    u32x4 out;
-                    out[0] = ra[0]; out[1] = rb[0]; out[2] = ra[1]; out[3] = rb[1];
-                    const int c = jb * 4 + gp + fr_half;                // 8-column chunk in the wave tile
-                    if (loader) {
-                        *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = out;
-                    } else if (row_ok) {
-                        *reinterpret_cast<u32x4*>(crow + 8 * c) = out;
-                    }
-                }
-            }
-        }
-        block_barrier();                                                // staging written
-        if (!loader) {
-            // storer wave w writes the staged tile of loader wave w - NL
-            const int lw = wave - NL;
-            const int lwm = lw / WAVES_N, lwn = lw % WAVES_N;
-            const uint8_t* stg = staging + lw * STG_B;
-            const int l_c0 = GATEUP ? cur_nt * (BN / 2) + lwn * (WN / 2) : cur_nt * BN + lwn * WN;
-            constexpr int ROWS_PER_READ = 1024 / OUT_RB;
-#pragma unroll
-            for (int r0 = 0; r0 < WM; r0 += ROWS_PER_READ) {
-                if (lwm * WM + r0 >= cur_rows) break;                   // wave-uniform
-                const int r = r0 + lane / OUT_CH;
-                const int c = lane % OUT_CH;
-                const u32x4 vv = *reinterpret_cast<const u32x4*>(stg + r * OUT_RB + 16 * (c ^ stg_swz(r)));
-                if (lwm * WM + r < cur_rows)
-                    *reinterpret_cast<u32x4*>(C + static_cast<size_t>(cur_row0 + lwm * WM + r) * N_out + l_c0 + 8 * c) = vv;
-            }
-        }
+        if (next < total) start_tile(next);
+        store_tile<GATEUP>(acc, C, N_out, cur_row0, cur_rows, cur_nt, wave, lane, lds + kStageBytes);
         tile = next;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// ------------------------------------------------------------------ fused bf16 FFN
+// Both GEMMs in one persistent kernel (calls of many m-tiles).  The m-tiles
+// (256 expert-sorted rows) are split into one contiguous range per XCD; a
+// workgroup reads its XCD from the XCC_ID hardware register.  Each XCD has a
+// queue: the gate/up tiles of its m-tiles, then their down tiles, claimed one
+// at a time through an atomic counter.  A down tile reads the H rows of its
+// m-tile, which gate/up tiles of the same XCD wrote: those stores are in that
+// XCD's L2, which its loads read.  Each storer wave adds 1 to its m-tile's
+// ready counter once its store counter has drained after a gate/up tile; a
+// down tile starts when that counter reaches (gate/up n-tiles) x (storer
+// waves).  The gate/up tail thereby overlaps the first down tiles, and each
+// XCD reads the weights of only the experts its rows belong to.
+//
+// The next queue entry is claimed during a tile's first stage, published at
+// its second and, for a down tile, its readiness polled two stages before the
+// end; a ready tile's first stage is issued before the epilogue, as in the
+// two-kernel path.  Counts of this tile's stores are delivered during the next
+// tile's second stage, or before any wait.
+//
+// No wait can deadlock: a workgroup waits (before a down tile) only once every
+// gate/up tile of its XCD's queue has been claimed; a gate/up tile is claimed
+// only by a running workgroup and never waits, and a workgroup delivers its own
+// pending counts before it waits.  Each wait is also bounded (kSpinLimit
+// polls): past it the kernel adds 1 to the error word and goes on.  A queue no
+// workgroup touched (an XCD that ran none of them) is run by the last
+// workgroup to finish, so every tile is computed whatever the dispatch.
+//
+// sync (ints, zero at launch): the queue counter of XCD x at
+// x * kSyncQueueStride, the error word, the finished-workgroup count, then
+// one ready counter per m-tile.
+constexpr int kSyncQueueStride = 32;                 // one 128-byte line per queue counter
+constexpr int kMaxXcc = 8;
+constexpr int kSyncErr = kMaxXcc * kSyncQueueStride;
+constexpr int kSyncDone = kSyncErr + 1;
+constexpr int kSyncReady = kSyncErr + kSyncQueueStride;
+constexpr int kSpinLimit = 1 << 20;
+
+__device__ __forceinline__ int xcc_register() {
+    int x;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(x));
+    return x;
+}
+
+__device__ __forceinline__ int atomic_add_agent(int* p, int v) {
+    return __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <bool GATHER>
+__global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W1, const uint16_t* __restrict__ W3,
+    const uint16_t* __restrict__ W2, uint16_t* __restrict__ H, uint16_t* __restrict__ Y,
+    const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int d, int inter,
+    const int32_t* __restrict__ row_src, int x_rows, int n_xcc, int* __restrict__ sync) {
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
+    __shared__ int mt_prefix[kMaxExpertsLocal + 1];
+    __shared__ int row_begin[kMaxExpertsLocal];
+    __shared__ int row_end[kMaxExpertsLocal];
+    // LDS broadcasts, one slot per value: each is written by one wave before a
+    // barrier and read after it, and not written again before another barrier
+    __shared__ int bcast[4];                // next entry; may it start early; finished count; untouched queue
+
+    build_schedule<kBM>(row_offsets, E_loc, max_rows, mt_prefix, row_begin, row_end);
+    const int MT = mt_prefix[E_loc];
+    const int n_gu = inter / (kBN / 2), n_dn = d / kBN;
+    const int target = n_gu * (kNW - kNL);
+    int* const ready = sync + kSyncReady;
+    const int lane = threadIdx.x % kWave;
+    const int wave = static_cast<int>(__builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
+    const bool loader = wave < kNL;
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
+    const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
+    const LaneMap lm = lane_map(lane);
+
+    // queue of XCD slot x: m-tiles [mb, me); gate/up entries [0, GU), down [GU, Q)
+    int x = xcc_register() % n_xcc;
+    int mb = 0, GU = 0, Q = 0;
+    int* queue = sync;
+    auto set_queue = [&](int xs) {
+        mb = (xs * MT) / n_xcc;
+        const int me = ((xs + 1) * MT) / n_xcc;
+        GU = (me - mb) * n_gu;
+        Q = GU + (me - mb) * n_dn;
+        queue = sync + xs * kSyncQueueStride;
+    };
+
+    struct Tile { int gu, m, nt, row0, rows, KT; };
+    Tile T{};
+    TileSrc src;
+    uint32_t lane_off[2] = {0, 0};
+    uint32_t a_off[kALd];
+    auto decode = [&](int t) {
+        Tile D;
+        D.gu = t < GU ? 1 : 0;
+        const int u = D.gu ? t : t - GU;
+        const int nn = D.gu ? n_gu : n_dn;
+        D.m = __builtin_amdgcn_readfirstlane(mb + u / nn);
+        D.nt = __builtin_amdgcn_readfirstlane(u % nn);
+        D.KT = (D.gu ? d : inter) / kStageK;
+        const int l = __builtin_amdgcn_readfirstlane(find_expert(mt_prefix, E_loc, D.m));
+        D.row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (D.m - mt_prefix[l]) * kBM);
+        D.rows = __builtin_amdgcn_readfirstlane(min(kBM, row_end[l] - D.row0));
+        if (loader) {
+            src = D.gu ? tile_src(true, GATHER, X, W1, W3, l, D.row0, D.rows, D.nt, wave, d, inter)
+                       : tile_src(false, false, H, W2, nullptr, l, D.row0, D.rows, D.nt, wave, inter, d);
+            lane_offsets(src, lm, lane_off);
+            if (GATHER && D.gu) gather_offsets(src, lm, wave, D.row0, row_src, x_rows, a_off);
+        }
+        return D;
+    };
+    auto issue = [&](int kt) {
+        if (loader) issue_stage(src, kt, wave, lm, lane_off, GATHER && T.gu, a_off, lds_base);
+    };
+    // wave 0 waits until m-tile m's H rows are complete, then the workgroup goes on
+    auto wait_ready = [&](int m) {
+        if (wave == 0 && lane == 0) {
+            int polls = 0;
+            while (atomic_add_agent(ready + m, 0) < target) {
+                if (++polls > kSpinLimit) {
+                    atomic_add_agent(sync + kSyncErr, 1);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(4);
+            }
+        }
+        block_barrier();
+    };
+    // a storer wave counts its drained gate/up stores on the m-tile's counter
+    int pending = -1;
+    auto deliver = [&]() {
+        if (!loader && pending >= 0) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            if (lane == 0) atomic_add_agent(ready + pending, 1);
+            pending = -1;
+        }
+    };
+    auto claim_blocking = [&]() {
+        if (wave == kNL && lane == 0) bcast[0] = atomic_add_agent(queue, 1);
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        block_barrier();
+        return __builtin_amdgcn_readfirstlane(bcast[0]);
+    };
+
+    bool checked_others = false;
+    set_queue(x);
+    for (;;) {
+        int t = claim_blocking();
+        if (t < Q) {
+            T = decode(t);
+            if (!T.gu) wait_ready(T.m);
+            issue(0);
+        }
+        while (t < Q) {
+            f32x16 acc[kMI][kNJ];
+#pragma unroll
+            for (int i = 0; i < kMI; ++i)
+#pragma unroll
+                for (int j = 0; j < kNJ; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+            const int KT = T.KT;
+            const bool ahead = KT >= 4;            // claim, publish and poll inside the K loop
+            int claim = 0, poll = 0;
+            for (int kt = 0; kt < KT; ++kt) {
+                if (loader) wait_vmem(0);
+                block_barrier();
+                if (kt + 1 < KT) issue(kt + 1);
+                if (ahead) {
+                    if (kt == 0 && wave == kNL && lane == 0) claim = atomic_add_agent(queue, 1);
+                    if (kt == 1) {
+                        deliver();
+                        if (wave == kNL && lane == 0) bcast[0] = claim;
+                    }
+                    if (kt == KT - 2 && wave == 0) {
+                        const int nx = bcast[0];
+                        if (nx >= GU && nx < Q && lane == 0) poll = atomic_add_agent(ready + mb + (nx - GU) / n_dn, 0);
+                    }
+                }
+                const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
+                mma_stage(sa, sa + kBM * kRowB, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, acc);
+            }
+            if (ahead && wave == 0 && lane == 0) {
+                const int nx = bcast[0];
+                bcast[1] = (nx < GU || nx >= Q || poll >= target) ? 1 : 0;
+            }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            block_barrier();                       // every wave is done with this tile's LDS
+            if (!ahead) {
+                deliver();
+                if (wave == kNL && lane == 0) {
+                    bcast[0] = atomic_add_agent(queue, 1);
+                    bcast[1] = 0;
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                block_barrier();
+            }
+            const int nx = __builtin_amdgcn_readfirstlane(bcast[0]);
+            const int early = __builtin_amdgcn_readfirstlane(bcast[1]) | (nx < GU ? 1 : 0);
+            const Tile C = T;
+            if (nx < Q) {
+                T = decode(nx);
+                if (early) issue(0);
+            }
+            if (C.gu) store_tile<true>(acc, H, inter, C.row0, C.rows, C.nt, wave, lane, lds + kStageBytes);
+            else store_tile<false>(acc, Y, d, C.row0, C.rows, C.nt, wave, lane, lds + kStageBytes);
+            if (C.gu) pending = C.m;
+            if (nx < Q && !early) {
+                deliver();                         // the next tile may need this tile's rows
+                wait_ready(T.m);
+                issue(0);
+            }
+            t = nx;
+        }
+        deliver();
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // The last workgroup to finish runs any queue that none touched.
+        if (!checked_others) {
+            checked_others = true;
+            if (wave == 0 && lane == 0) bcast[2] = atomic_add_agent(sync + kSyncDone, 1);
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            block_barrier();
+            if (__builtin_amdgcn_readfirstlane(bcast[2]) != static_cast<int>(gridDim.x) - 1) break;
+        }
+        if (wave == 0 && lane == 0) {
+            int found = -1;
+            for (int xs = 0; xs < n_xcc && found < 0; ++xs)
+                if (atomic_add_agent(sync + xs * kSyncQueueStride, 0) == 0) found = xs;
+            bcast[3] = found;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        block_barrier();
+        x = __builtin_amdgcn_readfirstlane(bcast[3]);
+        if (x < 0) break;
+        set_queue(x);
+    }
+}
+
+// Zeroes the fused kernel's counters (a kernel rather than a memset, so that
+// captured graphs hold no memset node).
+__global__ __launch_bounds__(256) void zero_ints_kernel(int* __restrict__ p, int n) {
+    for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0;
 }
 
 // ------------------------------------------------------------------ fp32 SIMT GEMM (small shapes)
@@ -562,9 +842,6 @@ __global__ __launch_bounds__(256) void ffn_gemm_f32_kernel(
     }
 }
 
-// Tile configurations (bf16).
-constexpr int kBM = 256, kBN = 256, kWavesM = 4, kWavesN = 2;
-
 int persistent_grid(long long tiles_upper) {
     const long long cus = device_cu_count();
     long long g = tiles_upper < cus ? tiles_upper : cus;
@@ -572,10 +849,23 @@ int persistent_grid(long long tiles_upper) {
     return static_cast<int>(g < 1 ? 1 : g);
 }
 
+// Row capacity from which a bf16 call runs the fused kernel: 32 m-tiles, so
+// that every XCD gets several; below it the two-kernel path spreads the few
+// m-tiles' n-tiles over all CUs.
+constexpr int kFusedMinRows = 32 * kBM;
+
+int fused_sync_ints(int max_rows) { return kSyncReady + (max_rows + kBM - 1) / kBM + kMaxExpertsLocal + 1; }
+
+size_t ffn_h_bytes(int max_rows, int inter, cap_dtype dt) {
+    const size_t h = static_cast<size_t>(max_rows) * inter * (dt == CAP_DTYPE_BF16 ? 2 : 4);
+    return (h + 255) & ~static_cast<size_t>(255);
+}
+
 }  // namespace
 
+// Workspace: H [max_rows][inter], then (bf16) the fused kernel's counters.
 size_t ffn_workspace_bytes(int max_rows, int inter, cap_dtype dt) {
-    return static_cast<size_t>(max_rows) * inter * (dt == CAP_DTYPE_BF16 ? 2 : 4);
+    return ffn_h_bytes(max_rows, inter, dt) + (dt == CAP_DTYPE_BF16 ? sizeof(int) * fused_sync_ints(max_rows) : 0);
 }
 
 cap_status ffn_supported(cap_dtype dt, int d, int inter) {
@@ -589,22 +879,45 @@ cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_
                              const int32_t* row_src, const int32_t* row_offsets, const void* w1, const void* w3,
                              const void* w2, void* y, void* ws, hipStream_t st) {
     if (dt == CAP_DTYPE_BF16) {
+        const auto* a = static_cast<const uint16_t*>(xs);
+        const auto* b1 = static_cast<const uint16_t*>(w1);
+        const auto* b3 = static_cast<const uint16_t*>(w3);
+        const auto* b2 = static_cast<const uint16_t*>(w2);
+        auto* h = static_cast<uint16_t*>(ws);
+        auto* out = static_cast<uint16_t*>(y);
+        const int n_xcc = device_xcc_count();
+        if (max_rows >= kFusedMinRows && n_xcc <= kMaxXcc) {
+            int* sync = reinterpret_cast<int*>(static_cast<char*>(ws) + ffn_h_bytes(max_rows, inter, dt));
+            zero_ints_kernel<<<1, 256, 0, st>>>(sync, fused_sync_ints(max_rows));
+            CAP_LAUNCH_CHECK();
+            int g = persistent_grid(1ll << 30);
+            // CAP_FFN_FUSED_GRID=n caps the grid (testing: with fewer
+            // workgroups than XCDs the last one runs the untouched queues)
+            if (const char* e = std::getenv("CAP_FFN_FUSED_GRID")) {
+                const int v = std::atoi(e);
+                if (v > 0 && v < g) g = v;
+            }
+            if (row_src)
+                ffn_fused_bf16_kernel<true><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
+                                                                       max_rows, d, inter, row_src, x_rows, n_xcc, sync);
+            else
+                ffn_fused_bf16_kernel<false><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
+                                                                        max_rows, d, inter, nullptr, 0, n_xcc, sync);
+            CAP_LAUNCH_CHECK();
+            return CAP_OK;
+        }
         const long long mt_upper = (static_cast<long long>(max_rows) + kBM - 1) / kBM + E_loc;
         const int g1 = persistent_grid(mt_upper * (inter / (kBN / 2)));
-        const auto* a = static_cast<const uint16_t*>(xs);
         if (row_src)
-            ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true, true><<<g1, kWavesM * kWavesN * kWave, 0, st>>>(
-                a, static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3), static_cast<uint16_t*>(ws),
-                row_offsets, E_loc, max_rows, d, inter, row_src, x_rows);
+            ffn_gemm_bf16_kernel<true, true><<<g1, kNW * kWave, 0, st>>>(a, b1, b3, h, row_offsets, E_loc, max_rows, d,
+                                                                         inter, row_src, x_rows);
         else
-            ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, true, false><<<g1, kWavesM * kWavesN * kWave, 0, st>>>(
-                a, static_cast<const uint16_t*>(w1), static_cast<const uint16_t*>(w3), static_cast<uint16_t*>(ws),
-                row_offsets, E_loc, max_rows, d, inter, nullptr, 0);
+            ffn_gemm_bf16_kernel<true, false><<<g1, kNW * kWave, 0, st>>>(a, b1, b3, h, row_offsets, E_loc, max_rows, d,
+                                                                          inter, nullptr, 0);
         CAP_LAUNCH_CHECK();
         const int g2 = persistent_grid(mt_upper * (d / kBN));
-        ffn_gemm_bf16_kernel<kBM, kBN, kWavesM, kWavesN, false, false><<<g2, kWavesM * kWavesN * kWave, 0, st>>>(
-            static_cast<const uint16_t*>(ws), static_cast<const uint16_t*>(w2), nullptr,
-            static_cast<uint16_t*>(y), row_offsets, E_loc, max_rows, inter, d, nullptr, 0);
+        ffn_gemm_bf16_kernel<false, false><<<g2, kNW * kWave, 0, st>>>(h, b2, nullptr, out, row_offsets, E_loc,
+                                                                       max_rows, inter, d, nullptr, 0);
         CAP_LAUNCH_CHECK();
     } else {
         const long long mt_upper = (static_cast<long long>(max_rows) + kF32Tile - 1) / kF32Tile + E_loc;

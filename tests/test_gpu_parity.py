@@ -345,6 +345,7 @@ def test_ffn_gather_equals_ffn_on_gathered_rows(name, kind, p):
 
 @pytest.mark.parametrize("dtype,d,inter,counts", [("bf16", 512, 384, [300, 1, 0, 513]),
                                                   ("bf16", 256, 128, [0, 700, 40]),
+                                                  ("bf16", 256, 128, [3000, 1, 0, 5200]),  # fused kernel
                                                   ("f32", 128, 256, [70, 0, 131])])
 def test_ffn_gather_ragged_with_repeats_and_clamping(dtype, d, inter, counts):
     """Ragged experts, repeated source rows and out-of-range indices (clamped
@@ -374,7 +375,7 @@ def test_ffn_gather_ragged_with_repeats_and_clamping(dtype, d, inter, counts):
 
 
 # ---------------------------------------------------------------- expert FFN
-def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0):
+def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0, max_rows=None):
     """cap_expert_ffn on synthetic ragged experts; returns (gpu Y, oracle Y)."""
     rng = np.random.default_rng(seed)
     rows = int(sum(counts))
@@ -391,7 +392,7 @@ def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0):
     else:
         tdt, cdt = torch.float32, capi.CAP_DTYPE_F32
         dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
-    max_rows = rows + 5
+    max_rows = rows + 5 if max_rows is None else max_rows
     xs = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
     xs[:rows] = dev(x32)
     y = torch.zeros((max_rows, d), dtype=tdt, device="cuda")
@@ -411,6 +412,89 @@ def test_ffn_bf16_ragged_experts(counts):
     ok, worst = C.within_tol(got, ref)
     assert ok, worst
     assert C.rel_fro(got, ref) <= 1e-2
+
+
+# Row capacity from which a bf16 call runs the fused kernel (both GEMMs in one
+# launch, a tile queue per XCD); below it the two-kernel path runs.
+FUSED_MIN_ROWS = 8192
+
+
+@pytest.mark.parametrize("d,inter,counts", [
+    (256, 128, [3000, 0, 1, 257, 4100, 0, 900, 2000]),   # down GEMM of two K stages
+    (512, 256, [9000]),                                   # every m-tile on one expert
+    (256, 384, [40] * 200 + [0] * 56),                    # 256 experts, one partial m-tile each
+    (256, 128, [100, 0, 200]),                            # two m-tiles: most XCD queues empty
+    (512, 384, []),                                       # no rows at all
+])
+def test_ffn_fused_ragged_experts(d, inter, counts):
+    counts = counts or [0, 0, 0]
+    rows = int(sum(counts))
+    got, ref = _ffn_direct("bf16", len(counts), d, inter, counts, seed=len(counts) + d,
+                           max_rows=max(FUSED_MIN_ROWS, rows + 5))
+    if rows == 0:
+        return
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+
+
+def test_ffn_fused_equals_two_kernel_path():
+    """The same rows with row capacities on either side of the fused kernel's
+    threshold give identical bits, and repeated fused calls (its counters are
+    cleared by every call) give the same bits again."""
+    rng = np.random.default_rng(5)
+    d, inter, counts = 512, 256, [700, 0, 1500, 3, 2000, 257]
+    E_loc, rows = len(counts), sum(counts)
+    offs = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32) + 4).cuda()
+    cdt = capi.CAP_DTYPE_BF16
+    bf = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).cuda()
+    w1 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w3 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w2 = bf(rng.standard_normal((E_loc, d, inter)) / (12 * np.sqrt(inter)))
+    x = bf(rng.standard_normal((FUSED_MIN_ROWS, d)))
+    outs = []
+    for max_rows in (FUSED_MIN_ROWS - 1, FUSED_MIN_ROWS, FUSED_MIN_ROWS):
+        ws = torch.full((capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),), 0xA5,
+                        dtype=torch.uint8, device="cuda")          # non-zero: the call clears its counters
+        y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+        for _ in range(2):
+            capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, x[:max_rows], offs, w1, w3, w2, y, ws)
+        torch.cuda.synchronize()
+        outs.append(y[:rows].view(torch.int16).cpu().numpy())
+    assert np.array_equal(outs[0], outs[1])
+    assert np.array_equal(outs[1], outs[2])
+
+
+@pytest.mark.parametrize("grid", [1, 3])
+def test_ffn_fused_with_fewer_workgroups_than_xcds(grid, monkeypatch):
+    """With the fused kernel's grid capped below the XCD count, the queues of
+    XCDs that ran no workgroup are run by the last workgroup to finish: the
+    result is still complete and identical to the full grid's."""
+    rng = np.random.default_rng(grid)
+    d, inter, counts = 256, 128, [2000, 0, 3000, 1, 4000]
+    E_loc, rows = len(counts), sum(counts)
+    max_rows = FUSED_MIN_ROWS + 100
+    offs = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)).cuda()
+    bf = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).cuda()
+    w1 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w3 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w2 = bf(rng.standard_normal((E_loc, d, inter)) / (12 * np.sqrt(inter)))
+    x = bf(rng.standard_normal((max_rows, d)))
+    cdt = capi.CAP_DTYPE_BF16
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                     dtype=torch.uint8, device="cuda")
+    outs = []
+    for cap in (None, grid):
+        if cap is None:
+            monkeypatch.delenv("CAP_FFN_FUSED_GRID", raising=False)
+        else:
+            monkeypatch.setenv("CAP_FFN_FUSED_GRID", str(cap))
+        y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+        capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, x, offs, w1, w3, w2, y, ws)
+        torch.cuda.synchronize()
+        outs.append(y[:rows].view(torch.int16).cpu().numpy())
+    monkeypatch.delenv("CAP_FFN_FUSED_GRID", raising=False)
+    assert np.array_equal(outs[0], outs[1])
 
 
 def test_ffn_f32_ragged_experts():
