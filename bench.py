@@ -345,7 +345,7 @@ def main():
     ffn_ms = sum(a.elapsed_time(b) for a, b in ffn_ev) / K
     log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
     eager_ms_per_step = ms_per_step
-    graph_ms_per_step = cold_ms_per_step = None
+    graph_ms_per_step = cold_ms_per_step = composite = None
     if graph is not None:
         # the same step captured once as a HIP graph and replayed K times
         for _ in range(args.warmup):
@@ -377,6 +377,33 @@ def main():
         cold_ms_per_step = float(np.median(cold))
         del flush
         log(f"cold-cache replays: {cold_ms_per_step:.4f} ms/step (median of {len(cold)})")
+        # the front end alone (route, layout, co-activation of all T tokens),
+        # for the composite rank-0 rate that charges rank 0 its 1/R share of it
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
+            L.front(side=side)
+        stream.wait_stream(cap)
+        fg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(fg):
+            L.front(side=side)
+        for _ in range(args.warmup):
+            fg.replay()
+        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        f0.record(stream)
+        for _ in range(K):
+            fg.replay()
+        f1.record(stream)
+        torch.cuda.synchronize()
+        front_ms = f0.elapsed_time(f1) / K
+        composite = {
+            "front_graph_ms": front_ms,
+            "rank0_step_ms": graph_ms_per_step - front_ms * (1.0 - 1.0 / cfg.R),
+            "tokens_per_s": cfg.tokens_per_rank / ((graph_ms_per_step - front_ms * (1.0 - 1.0 / cfg.R)) * 1e-3),
+            "definition": "tokens_per_rank / (step - (1 - 1/R) * front end): rank 0's own share of routing, "
+                          "layout and co-activation plus its whole rank path",
+        }
+        log(f"front end alone: {front_ms:.4f} ms; composite rank-0 rate {composite['tokens_per_s'] / 1e6:.2f} M tokens/s")
 
     # per-stage breakdown (separate, untimed pass)
     stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
@@ -487,6 +514,7 @@ def main():
             "host_wall_ms_per_step": 1e3 * wall / K,
             "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
             "cold_cache_ms_per_step": cold_ms_per_step,
+            "composite_rank0": composite,
         },
     }
     if not args.no_cpu:
