@@ -311,17 +311,9 @@ def main():
 
     def one_step(ev=None):
         """The whole hot path once: front end over all tokens, then rank r's
-        row source, gathered FFN, destination reduce, shared FFN, source reduce."""
-        L.front(side=side)
-        L.row_source(rank)
-        if ev is not None:
-            ev[0].record(stream)
-        L.ffn_gather(rank)
-        if ev is not None:
-            ev[1].record(stream)
-        L.dest_reduce(rank)
-        L.shared_ffn(rank)
-        L.src_reduce(rank)
+        row source, gathered FFN, destination reduce and source reduce, with
+        the shared experts and the co-activation counts on the side stream."""
+        L.step(rank, side=side, ffn_events=ev)
 
     # the graph is captured first, so that the eager loop, the graph warmup
     # and the timed replays follow each other without an idle gap

@@ -210,25 +210,62 @@ class DeviceLayer:
         self.src_reduce(rank, stream)
 
     def capture_step(self, rank: int = 0, side=None, warmup: int = 2) -> torch.cuda.CUDAGraph:
-        """The whole step (front end, then rank `rank`'s path) as one HIP graph.
+        """The whole step (step(rank, side=side)) as one HIP graph.
         Every call writes fixed buffers and allocates nothing, so replays redo
         exactly the eager work."""
         cap = torch.cuda.Stream()
         cap.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(cap):
             for _ in range(warmup):
-                self.front(side=side)
-                self.rank_path(rank)
+                self.step(rank, side=side)
         torch.cuda.current_stream().wait_stream(cap)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            self.front(side=side)
-            self.rank_path(rank)
+            self.step(rank, side=side)
         return g
 
-    def step(self, rank: int = 0, stream=None):
-        self.front(stream)
-        self.rank_path(rank, stream)
+    def step(self, rank: int = 0, stream=None, side=None, ffn_events=None):
+        """One layer step: the front end over all virtual ranks' tokens, then
+        rank `rank`'s path.  With a side stream, the work that no later
+        main-stream kernel reads runs there: the shared experts (they read only
+        x) from the start of the step, the co-activation counts once routing
+        is done; the main stream joins it before the source reduce, which adds
+        the shared output.  ffn_events: an optional pair of events recorded on
+        the main stream around the routed FFN."""
+        main = stream if stream is not None else torch.cuda.current_stream()
+        if side is not None:
+            if not hasattr(self, "_step_ev"):
+                self._step_ev = [torch.cuda.Event() for _ in range(3)]
+            start, routed, side_done = self._step_ev
+            start.record(main)
+            side.wait_event(start)
+            self.shared_ffn(rank, side)
+            self.route(main)
+            routed.record(main)
+            side.wait_event(routed)
+            self.coactivation(False, side)
+            side_done.record(side)
+            self.layout(main)
+        else:
+            self.front(main)
+        if self.fused_gather:
+            self.row_source(rank, main)
+        else:
+            self.gather(rank, main)
+        if ffn_events is not None:
+            ffn_events[0].record(main)
+        if self.fused_gather:
+            self.ffn_gather(rank, main)
+        else:
+            self.ffn(rank, main)
+        if ffn_events is not None:
+            ffn_events[1].record(main)
+        self.dest_reduce(rank, main)
+        if side is not None:
+            main.wait_event(side_done)
+        else:
+            self.shared_ffn(rank, main)
+        self.src_reduce(rank, main)
 
     # ------------------------------------------------------------ host views
     def host(self, name: str) -> np.ndarray:

@@ -108,6 +108,42 @@ def test_front_with_side_stream_matches_serial(case):
         assert np.array_equal(L.host(n), v), n
 
 
+@pytest.mark.parametrize("name", ["c4", "c2"])
+def test_step_with_side_stream_matches_serial(name):
+    """The step with the shared experts and the co-activation counts on a side
+    stream (joined before the source reduce) gives the serial step's bits."""
+    case = C.Case(name, gen.CONFIGS[name], "coact", 0.1)
+    cfg = case.cfg
+    er, el = C.placement(name, "coact", 0.1, 5.0)
+    L = _layer(case, x=gen.activations(cfg))
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    if cfg.n_shared:
+        L.set_shared_weights(*gen.shared_weights(cfg))
+    g0 = torch.Generator(device="cuda").manual_seed(3)
+    L.parts.copy_((torch.randn(L.parts.shape, generator=g0, device="cuda") * 0.05).to(L.tdt))
+    L.step(0)
+    torch.cuda.synchronize()
+    rows = L.rank_rows(0)
+    names = ("y", "Y", "coact", "shared_out") if cfg.n_shared else ("y", "Y", "coact")
+
+    def snap(n):
+        v = L.host(n)
+        return v[:rows].copy() if n == "Y" else v.copy()
+
+    want = {n: snap(n) for n in names}
+    side = torch.cuda.Stream()
+    for rep in range(2):
+        L.y.zero_()
+        L.Y.zero_()
+        L.coact.zero_()
+        if cfg.n_shared:
+            L.shared_out.zero_()
+        L.step(0, side=side)
+        torch.cuda.synchronize()
+        for n in names:
+            assert np.array_equal(snap(n).view(np.uint8), want[n].view(np.uint8)), (rep, n)
+
+
 def _check_router_route(L, cfg, x_bits, wg_bits, er, rows=None):
     """Fused router + routing: the decisions equal the logits-in kernel's (and
     the oracle's) on the logits the fused kernel used, and those logits equal
