@@ -307,7 +307,10 @@ def main():
     log(f"setup {time.perf_counter() - t_setup:.1f} s; rank-{rank} rows {L.rank_rows(rank)}, received rows {n_recv}")
 
     stream = torch.cuda.current_stream()
-    side = torch.cuda.Stream()            # co-activation beside the layout (default priority)
+    # a side stream for the shared experts and the co-activation counts when
+    # there are shared experts; without them the co-activation counts run in
+    # line (in a replayed graph each dependency between streams costs ~10 us)
+    side = torch.cuda.Stream() if cfg.n_shared else None
 
     def one_step(ev=None):
         """The whole hot path once: front end over all tokens, then rank r's
