@@ -410,6 +410,46 @@ def test_ffn_gather_ragged_with_repeats_and_clamping(dtype, d, inter, counts):
     assert torch.equal(y[:rows].view(torch.uint8), y_ref[:rows].view(torch.uint8))
 
 
+# Row capacity from which a bf16 call runs the fused kernel (both GEMMs in one
+# launch, a tile queue per XCD); below it the two-kernel path runs.
+FUSED_MIN_ROWS = 8192
+
+
+def test_ffn_gather_offsets_near_4gib():
+    """Gathered rows at the far end of an x of just under 4 GiB (the limit the
+    C ABI states: x_rows * d * 2 < 2^32): the 32-bit byte offsets of the
+    gathered loads reach the last rows exactly; the result equals the FFN on
+    the explicitly gathered rows, on the fused kernel's path (row capacity
+    >= 8192) and on the two-kernel path."""
+    d, inter = 2048, 256
+    x_rows = (1 << 32) // (d * 2) - 1                       # 1,048,575 rows, 4 GiB - 4 KiB
+    counts = [3000, 0, 2000, 3100]                           # 8100 rows: < 8192 for the two-kernel path
+    E_loc, rows = len(counts), sum(counts)
+    g = torch.Generator(device="cuda").manual_seed(17)
+    x = torch.randn((x_rows, d), generator=g, device="cuda").to(torch.bfloat16)
+    src = torch.randint(x_rows - 20000, x_rows, (rows,), generator=g, device="cuda", dtype=torch.int32)
+    src[:8] = x_rows - 1                                     # the very last row
+    offs = torch.tensor(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32), device="cuda")
+    w1 = (torch.randn((E_loc, inter, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    w3 = (torch.randn((E_loc, inter, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    w2 = (torch.randn((E_loc, d, inter), generator=g, device="cuda") / (12 * inter ** 0.5)).to(torch.bfloat16)
+    cdt = capi.CAP_DTYPE_BF16
+    for max_rows in (FUSED_MIN_ROWS + 64, rows):
+        row_src = torch.zeros(max_rows, dtype=torch.int32, device="cuda")
+        row_src[:rows] = src
+        xs = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+        xs[:rows] = x[src.long()]
+        ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                         dtype=torch.uint8, device="cuda")
+        y_ref = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+        y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+        capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, xs, offs, w1, w3, w2, y_ref, ws)
+        capi.cap_expert_ffn_gather(cdt, E_loc, d, inter, max_rows, x, x_rows, row_src, offs, w1, w3, w2, y, ws)
+        torch.cuda.synchronize()
+        assert torch.equal(y[:rows].view(torch.int16), y_ref[:rows].view(torch.int16)), max_rows
+    del x
+
+
 # ---------------------------------------------------------------- expert FFN
 def _ffn_direct(dtype, E_loc, d, inter, counts, seed=0, max_rows=None):
     """cap_expert_ffn on synthetic ragged experts; returns (gpu Y, oracle Y)."""
@@ -448,11 +488,6 @@ def test_ffn_bf16_ragged_experts(counts):
     ok, worst = C.within_tol(got, ref)
     assert ok, worst
     assert C.rel_fro(got, ref) <= 1e-2
-
-
-# Row capacity from which a bf16 call runs the fused kernel (both GEMMs in one
-# launch, a tile queue per XCD); below it the two-kernel path runs.
-FUSED_MIN_ROWS = 8192
 
 
 @pytest.mark.parametrize("d,inter,counts", [
