@@ -2,18 +2,21 @@
 """Benchmark of the CAP expert-parallel MoE layer hot path on one MI355X.
 
 One step = the whole hot path over one batch of synthetic input, inputs
-resident in HBM:
+resident in HBM (DeviceLayer.step):
   route + prune (all T tokens of all virtual ranks), dispatch layout,
-  co-activation counts, expert gather for rank 0, rank 0's grouped SwiGLU FFN,
-  destination reduce for rank 0, [shared experts], source reduce for rank 0.
+  co-activation counts, rank 0's row source (the expert gather as indices),
+  rank 0's grouped SwiGLU FFN reading x rows in place, destination reduce for
+  rank 0, [shared experts, on a side stream], source reduce for rank 0.
+The step is captured once as a HIP graph and replayed; --warmup untimed steps
+(eager and replayed) let the GPU clock settle before --steps timed ones.
 `value` = rank 0's tokens carried through the layer per second
 (tokens_per_rank / step time; the step also routes every other virtual rank's
 tokens, which a real rank would not do).
 
 The rows every other rank returns to rank 0 are stand-in values in HBM (on a
 real system they arrive by all-to-all); rank 0's own rows are recomputed every
-step.  The dominant kernel is the grouped FFN (two GEMM launches per call),
-timed live with HIP events on the stream it runs on.
+step.  The dominant kernel is the grouped FFN (one fused launch for both GEMMs
+on the bench workloads), timed live with HIP events on the stream it runs on.
 """
 from __future__ import annotations
 

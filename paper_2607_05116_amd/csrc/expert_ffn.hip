@@ -100,7 +100,7 @@ __device__ __forceinline__ const void* uniform_ptr(const void* p) {
 // instruction's immediate offset stays 0 (it would shift the LDS address too).
 // They are inline assembly so that the compiler's wait-count pass does not
 // treat every later LDS read as aliasing them (it would drain all in-flight
-// stages); the kernel waits on them explicitly with wait_vmem().  Because the
+// stages); the kernel waits on them explicitly with wait_loads().  Because the
 // compiler does not see the instruction, it also does not insert the wait
 // states the hardware needs before it: a VALU write of an SGPR (v_readfirstlane
 // of the base) needs 5 wait states before a vector-memory instruction reads it,
@@ -161,39 +161,20 @@ __device__ __forceinline__ int lds_swz(int r) { return (r & 7) ^ ((r >> 3) & 1);
 
 // Workgroup barrier without the memory fence that __syncthreads() carries (the
 // fence would drain every in-flight prefetch).  LDS visibility is ensured by
-// explicit vmcnt waits on the direct-to-LDS loads and the compiler's lgkmcnt
-// waits on ds_read; the empty asm statements keep memory accesses from being
-// moved across the barrier.
+// explicit waits: vmcnt for the direct-to-LDS loads, and lgkmcnt(0) before a
+// barrier that publishes ds_write data (staged outputs, broadcast values); the
+// empty asm statements keep memory accesses from being moved across the
+// barrier.
 __device__ __forceinline__ void block_barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
 
-// Wait until at most n of this wave's vector-memory operations are in flight
-// (n rounded down to a multiple of 4, at most 60).  Vector-memory operations
-// complete in issue order, so with n = (operations issued after the stage we
-// need) that stage has landed in LDS; waiting for fewer is only stricter.
-__device__ __forceinline__ void wait_vmem(int n) {
-    switch (n >= 60 ? 15 : n >> 2) {
-        case 15: asm volatile("s_waitcnt vmcnt(60)" ::: "memory"); break;
-        case 14: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
-        case 13: asm volatile("s_waitcnt vmcnt(52)" ::: "memory"); break;
-        case 12: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
-        case 11: asm volatile("s_waitcnt vmcnt(44)" ::: "memory"); break;
-        case 10: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
-        case 9: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
-        case 8: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
-        case 7: asm volatile("s_waitcnt vmcnt(28)" ::: "memory"); break;
-        case 6: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
-        case 5: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
-        case 4: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-        case 3: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-        case 2: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-        case 1: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-        default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    }
-}
+// Wait until every vector-memory operation of this wave has completed: its
+// direct-to-LDS loads have landed in LDS (the compiler does not see them, so
+// it inserts no wait of its own).
+__device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -507,7 +488,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
         for (int kt = 0; kt < KT; ++kt) {
-            if (loader) wait_vmem(0);              // this wave's part of stage kt has landed
+            if (loader) wait_loads();              // this wave's part of stage kt has landed
             block_barrier();                       // stage kt visible; the other buffer is free
             if (loader && kt + 1 < KT) issue_stage(src, kt + 1, wave, lm, lane_off, GATHER, a_off, lds_base);
             const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
@@ -690,7 +671,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
             const bool ahead = KT >= 4;            // claim, publish and poll inside the K loop
             int claim = 0, poll = 0;
             for (int kt = 0; kt < KT; ++kt) {
-                if (loader) wait_vmem(0);
+                if (loader) wait_loads();
                 block_barrier();
                 if (kt + 1 < KT) issue(kt + 1);
                 if (ahead) {

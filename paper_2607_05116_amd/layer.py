@@ -197,17 +197,30 @@ class DeviceLayer:
         self.layout(main)
         main.wait_event(self._join)
 
-    def rank_path(self, rank: int, stream=None):
-        """The destination and source work of one rank."""
+    def rank_path(self, rank: int, stream=None, ffn_events=None, join=None):
+        """The destination and source work of one rank.  ffn_events: an
+        optional pair of events recorded around the routed FFN.  join: an event
+        the source reduce waits for, when the shared experts ran on another
+        stream; without it they run here, before the source reduce."""
+        main = stream if stream is not None else torch.cuda.current_stream()
         if self.fused_gather:
-            self.row_source(rank, stream)
-            self.ffn_gather(rank, stream)
+            self.row_source(rank, main)
         else:
-            self.gather(rank, stream)
-            self.ffn(rank, stream)
-        self.dest_reduce(rank, stream)
-        self.shared_ffn(rank, stream)
-        self.src_reduce(rank, stream)
+            self.gather(rank, main)
+        if ffn_events is not None:
+            ffn_events[0].record(main)
+        if self.fused_gather:
+            self.ffn_gather(rank, main)
+        else:
+            self.ffn(rank, main)
+        if ffn_events is not None:
+            ffn_events[1].record(main)
+        self.dest_reduce(rank, main)
+        if join is None:
+            self.shared_ffn(rank, main)
+        else:
+            main.wait_event(join)
+        self.src_reduce(rank, main)
 
     def capture_step(self, rank: int = 0, side=None, warmup: int = 2) -> torch.cuda.CUDAGraph:
         """The whole step (step(rank, side=side)) as one HIP graph.
@@ -230,42 +243,25 @@ class DeviceLayer:
         main-stream kernel reads runs there: the shared experts (they read only
         x) from the start of the step, the co-activation counts once routing
         is done; the main stream joins it before the source reduce, which adds
-        the shared output.  ffn_events: an optional pair of events recorded on
-        the main stream around the routed FFN."""
+        the shared output.  ffn_events: as in rank_path."""
         main = stream if stream is not None else torch.cuda.current_stream()
-        if side is not None:
-            if not hasattr(self, "_step_ev"):
-                self._step_ev = [torch.cuda.Event() for _ in range(3)]
-            start, routed, side_done = self._step_ev
-            start.record(main)
-            side.wait_event(start)
-            self.shared_ffn(rank, side)
-            self.route(main)
-            routed.record(main)
-            side.wait_event(routed)
-            self.coactivation(False, side)
-            side_done.record(side)
-            self.layout(main)
-        else:
+        if side is None:
             self.front(main)
-        if self.fused_gather:
-            self.row_source(rank, main)
-        else:
-            self.gather(rank, main)
-        if ffn_events is not None:
-            ffn_events[0].record(main)
-        if self.fused_gather:
-            self.ffn_gather(rank, main)
-        else:
-            self.ffn(rank, main)
-        if ffn_events is not None:
-            ffn_events[1].record(main)
-        self.dest_reduce(rank, main)
-        if side is not None:
-            main.wait_event(side_done)
-        else:
-            self.shared_ffn(rank, main)
-        self.src_reduce(rank, main)
+            self.rank_path(rank, main, ffn_events)
+            return
+        if not hasattr(self, "_step_ev"):
+            self._step_ev = [torch.cuda.Event() for _ in range(3)]
+        start, routed, side_done = self._step_ev
+        start.record(main)
+        side.wait_event(start)
+        self.shared_ffn(rank, side)
+        self.route(main)
+        routed.record(main)
+        side.wait_event(routed)
+        self.coactivation(False, side)
+        side_done.record(side)
+        self.layout(main)
+        self.rank_path(rank, main, ffn_events, join=side_done)
 
     # ------------------------------------------------------------ host views
     def host(self, name: str) -> np.ndarray:
