@@ -267,7 +267,8 @@ cap_status cap_permute(const cap_topology *topo, cap_permute_mode mode, int32_t 
  * contents need no initialisation.
  * bf16 calls with max_rows >= 8192 run both GEMMs in one kernel with a tile
  * queue per XCD (a down tile starts once the gate/up tiles of its rows are
- * done); smaller calls run one kernel per GEMM.  Both give the same bits.
+ * done) on a device of 8 XCDs (or one); other calls run one kernel per GEMM.
+ * Both give the same bits.
  * The environment variable CAP_FFN_FUSED_GRID=n caps the fused kernel's grid
  * at n workgroups (for tests; the result does not change).
  */

@@ -866,8 +866,11 @@ cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_
         const auto* b2 = static_cast<const uint16_t*>(w2);
         auto* h = static_cast<uint16_t*>(ws);
         auto* out = static_cast<uint16_t*>(y);
+        // The fused kernel maps XCC_ID % n_xcc to a queue: with 8 XCCs the ids
+        // are 0..7 (one per XCD); with one XCC all CUs share one L2.  Other
+        // partitions take the two-kernel path, which needs no such mapping.
         const int n_xcc = device_xcc_count();
-        if (max_rows >= kFusedMinRows && n_xcc <= kMaxXcc) {
+        if (max_rows >= kFusedMinRows && (n_xcc == kMaxXcc || n_xcc == 1)) {
             int* sync = reinterpret_cast<int*>(static_cast<char*>(ws) + ffn_h_bytes(max_rows, inter, dt));
             zero_ints_kernel<<<1, 256, 0, st>>>(sync, fused_sync_ints(max_rows));
             CAP_LAUNCH_CHECK();
