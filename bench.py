@@ -343,7 +343,7 @@ def main():
     ffn_ms = sum(a.elapsed_time(b) for a, b in ffn_ev) / K
     log(f"timed {K} steps: {ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step), FFN {ffn_ms:.4f} ms")
     eager_ms_per_step = ms_per_step
-    graph_ms_per_step = cold_ms_per_step = composite = None
+    graph_ms_per_step = cold_ms_per_step = cold_dirty_ms_per_step = composite = None
     if graph is not None:
         # the same step captured once as a HIP graph and replayed K times
         for _ in range(args.warmup):
@@ -361,20 +361,28 @@ def main():
         ms_per_step = graph_ms_per_step
         log(f"graph replays: {graph_ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step)")
         # the same replays with the caches cold: 512 MB (twice the 256 MB
-        # Infinity Cache) rewritten before each, outside its timed window
+        # Infinity Cache) read before each, outside its timed window, which
+        # leaves the caches full of clean lines of other data; and the same
+        # after 512 MB are rewritten, whose dirty lines the step also writes back
         flush = torch.zeros(512 << 20, dtype=torch.uint8, device="cuda")
-        cold = []
-        for _ in range(min(K, 10)):
-            flush.add_(1)
-            c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            c0.record(stream)
-            graph.replay()
-            c1.record(stream)
-            torch.cuda.synchronize()
-            cold.append(c0.elapsed_time(c1))
-        cold_ms_per_step = float(np.median(cold))
+
+        def cold_replays(evict):
+            times = []
+            for _ in range(min(K, 10)):
+                evict()
+                c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                c0.record(stream)
+                graph.replay()
+                c1.record(stream)
+                torch.cuda.synchronize()
+                times.append(c0.elapsed_time(c1))
+            return float(np.median(times))
+
+        cold_ms_per_step = cold_replays(lambda: flush.sum(dtype=torch.int64))
+        cold_dirty_ms_per_step = cold_replays(lambda: flush.add_(1))
         del flush
-        log(f"cold-cache replays: {cold_ms_per_step:.4f} ms/step (median of {len(cold)})")
+        log(f"cold-cache replays: {cold_ms_per_step:.4f} ms/step after a 512 MB read, "
+            f"{cold_dirty_ms_per_step:.4f} after a 512 MB rewrite (medians of {min(K, 10)})")
         # the front end alone (route, layout, co-activation of all T tokens),
         # for the composite rank-0 rate that charges rank 0 its 1/R share of it
         cap = torch.cuda.Stream()
@@ -512,6 +520,7 @@ def main():
             "host_wall_ms_per_step": 1e3 * wall / K,
             "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
             "cold_cache_ms_per_step": cold_ms_per_step,
+            "cold_cache_dirty_ms_per_step": cold_dirty_ms_per_step,
             "composite_rank0": composite,
         },
     }
