@@ -411,23 +411,40 @@ def main():
         }
         log(f"front end alone: {front_ms:.4f} ms; composite rank-0 rate {composite['tokens_per_s'] / 1e6:.2f} M tokens/s")
 
-    # per-stage breakdown (separate, untimed pass)
+    # per-stage device times (separate, untimed): each stage captured as a graph
+    # of 20 back-to-back calls (every stage rewrites the same buffers from
+    # unchanged inputs) and replayed, so launch gaps do not enter the times
     stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
     fns = [L.route, L.layout, L.coactivation, lambda: L.row_source(rank), lambda: L.ffn_gather(rank),
            lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank),
            lambda: L.gather(rank), lambda: L.ffn(rank)]
-    reps = 5
-    acc = {s: 0.0 for s in stages}
-    for _ in range(reps):
-        evs = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
-        evs[0].record(stream)
-        for j, fn in enumerate(fns):
+
+    def stage_time(fn, n=20, reps=5):
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        with torch.cuda.stream(cap):
             fn()
-            evs[j + 1].record(stream)
+        stream.wait_stream(cap)
+        sg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(sg):
+            for _ in range(n):
+                fn()
+        sg.replay()
         torch.cuda.synchronize()
-        for j, s in enumerate(stages):
-            acc[s] += evs[j].elapsed_time(evs[j + 1]) / reps
-    stage_ms = {s: round(v, 5) for s, v in acc.items()}
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            sg.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (n * reps)
+
+    stage_ms = {}
+    for s_name, fn in zip(stages, fns):
+        if s_name == "shared" and not cfg.n_shared:
+            stage_ms[s_name] = 0.0
+            continue
+        stage_ms[s_name] = round(stage_time(fn), 5)
 
     rows = L.rank_rows(rank)
     flops = 6.0 * cfg.d * cfg.inter * rows
