@@ -536,6 +536,46 @@ def test_ffn_fused_equals_two_kernel_path():
     assert np.array_equal(outs[1], outs[2])
 
 
+def test_ffn_fused_repeated_calls_identical():
+    """Forty fused-kernel calls give the same bits each time, half of them
+    while a large elementwise kernel on another stream holds compute units
+    (workgroups then start late and unevenly, so the per-XCD queues and the
+    waits for an m-tile's H rows run in other orders)."""
+    rng = np.random.default_rng(9)
+    d, inter = 512, 256
+    counts = list(rng.integers(0, 2500, size=16))
+    E_loc, rows = len(counts), int(sum(counts))
+    max_rows = max(FUSED_MIN_ROWS, rows)
+    offs = torch.tensor(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32), device="cuda")
+    g = torch.Generator(device="cuda").manual_seed(9)
+    x = torch.randn((max_rows, d), generator=g, device="cuda").to(torch.bfloat16)
+    w1 = (torch.randn((E_loc, inter, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    w3 = (torch.randn((E_loc, inter, d), generator=g, device="cuda") / d ** 0.5).to(torch.bfloat16)
+    w2 = (torch.randn((E_loc, d, inter), generator=g, device="cuda") / (12 * inter ** 0.5)).to(torch.bfloat16)
+    cdt = capi.CAP_DTYPE_BF16
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                     dtype=torch.uint8, device="cuda")
+    y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+    capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, x, offs, w1, w3, w2, y, ws)
+    torch.cuda.synchronize()
+    want = y[:rows].clone()
+    want_sum = want.view(torch.int16).to(torch.int64).sum()
+    other = torch.cuda.Stream()
+    big = torch.zeros(1 << 28, dtype=torch.float32, device="cuda")
+    sums = []
+    for it in range(40):
+        y.zero_()
+        if it % 2:
+            with torch.cuda.stream(other):
+                big.add_(1.0)
+        capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, x, offs, w1, w3, w2, y, ws)
+        sums.append(y[:rows].view(torch.int16).to(torch.int64).sum())
+    torch.cuda.synchronize()
+    assert all(int(v) == int(want_sum) for v in sums), [int(v) for v in sums]
+    assert torch.equal(y[:rows].view(torch.int16), want.view(torch.int16))
+    del big
+
+
 @pytest.mark.parametrize("grid", [1, 3])
 def test_ffn_fused_with_fewer_workgroups_than_xcds(grid, monkeypatch):
     """With the fused kernel's grid capped below the XCD count, the queues of
