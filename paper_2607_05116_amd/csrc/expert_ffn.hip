@@ -678,7 +678,10 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
                     if (kt == 0 && wave == kNL && lane == 0) claim = atomic_add_agent(queue, 1);
                     if (kt == 1) {
                         deliver();
-                        if (wave == kNL && lane == 0) bcast[0] = claim;
+                        if (wave == kNL) {
+                            if (lane == 0) bcast[0] = claim;
+                            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // visible at the next barrier
+                        }
                     }
                     if (kt == KT - 2 && wave == 0) {
                         const int nx = bcast[0];
