@@ -481,6 +481,24 @@ def main():
     torch.cuda.synchronize()
     pruning["naive"] = volume(L.host("totals").astype(np.int64), int(L.host("keep").sum()))
     L.naive = False
+    # CAP's volumes over the pruning threshold (untimed), and on multi-node
+    # layers the same with c = 1 (the inter-node cost orders remote devices)
+    sweep = []
+    c_values = [args.c] + ([1.0] if cfg.R > cfg.ranks_per_node and args.c != 1.0 else [])
+    for cc in c_values:
+        L.topo.inter_node_cost = cc
+        for pp in (0.0, 0.05, 0.1, 0.2, 0.3):
+            L.p = pp
+            L.route()
+            L.layout()
+            torch.cuda.synchronize()
+            tot = L.host("totals").astype(np.int64)
+            v = volume(tot, int(L.host("keep").sum()))
+            v.update({"p": pp, "c": cc, "intra_copies_per_token": int(tot[1]) / cfg.T,
+                      "inter_copies_per_token": int(tot[2]) / cfg.T})
+            sweep.append(v)
+    L.topo.inter_node_cost = args.c
+    L.p = args.p
     L.route()
     L.layout()
     torch.cuda.synchronize()
@@ -531,6 +549,7 @@ def main():
             "node_per_token": int(totals[3]) / cfg.T,
             "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
             "pruning_cap_vs_naive": pruning,
+            "pruning_sweep": sweep,
             "placement_spectrum": spectrum,
             "fused_router_front_end": front_end,
             "rank_rows": rows, "rank_received_tokens": U,
