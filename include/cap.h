@@ -259,7 +259,7 @@ cap_status cap_permute(const cap_topology *topo, cap_permute_mode mode, int32_t 
  *   w1, w3 [E_loc][inter][d]; w2 [E_loc][d][inter] (K-contiguous rows).
  *   y[.][d]           output rows, same row order as xs.
  * bf16: fp32 accumulation, H rounded to bf16 between the two GEMMs, y bf16;
- *       needs d % 256 == 0 and inter % 128 == 0.
+ *       needs d % 256 == 0, inter % 128 == 0 and d, inter <= 2^19.
  * f32:  fp32 throughout; needs d % 4 == 0.
  * Shared experts: call with E_loc = 1, row_offsets = {0, n}, inter = the
  * concatenated intermediate size.  Workspace: cap_workspace_size(CAP_OP_EXPERT_FFN):

@@ -852,8 +852,12 @@ size_t ffn_workspace_bytes(int max_rows, int inter, cap_dtype dt) {
     return ffn_h_bytes(max_rows, inter, dt) + (dt == CAP_DTYPE_BF16 ? sizeof(int) * fused_sync_ints(max_rows) : 0);
 }
 
+// bf16: the direct loads form 8-row block offsets (16 K bytes) with 24-bit
+// multiplies, so K = d or inter stays below 2^20 (2^19 here).
 cap_status ffn_supported(cap_dtype dt, int d, int inter) {
-    if (dt == CAP_DTYPE_BF16) return (d % kBN == 0 && inter % (kBN / 2) == 0) ? CAP_OK : CAP_ERR_UNSUPPORTED;
+    if (dt == CAP_DTYPE_BF16)
+        return (d % kBN == 0 && inter % (kBN / 2) == 0 && d <= (1 << 19) && inter <= (1 << 19)) ? CAP_OK
+                                                                                              : CAP_ERR_UNSUPPORTED;
     return (d % 4 == 0) ? CAP_OK : CAP_ERR_UNSUPPORTED;
 }
 

@@ -110,6 +110,9 @@ def test_workspace_checks(capi):
 def test_ffn_rejects_unsupported_shapes(capi):
     args = (0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 0x6000, 0x7000, 1 << 30, None)
     assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2000, 768, 100, *args) == capi.CAP_ERR_UNSUPPORTED
+    # K beyond the 24-bit block offsets of the direct loads
+    assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 1 << 20, 768, 100, *args) == capi.CAP_ERR_UNSUPPORTED
+    assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2048, 1 << 20, 100, *args) == capi.CAP_ERR_UNSUPPORTED
     assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 4, 2048, 700, 100, *args) == capi.CAP_ERR_UNSUPPORTED
     assert capi._lib.cap_expert_ffn(7, 4, 2048, 768, 100, *args) == capi.CAP_ERR_UNSUPPORTED
     assert capi._lib.cap_expert_ffn(capi.CAP_DTYPE_BF16, 0, 2048, 768, 100, *args) == capi.CAP_ERR_INVALID_ARG
