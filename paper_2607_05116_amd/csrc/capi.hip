@@ -41,15 +41,16 @@ int device_cu_count() {
     return n;
 }
 
-// XCD (XCC) count of the current device, cached per device.
+// XCD (XCC) count of the current device, cached per device; 0 when the
+// runtime cannot tell (callers then take paths that do not depend on it).
 int device_xcc_count() {
     static std::atomic<int> cache[64];
     int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
     int v = cache[dev].load(std::memory_order_relaxed);
     if (v > 0) return v;
     int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || n <= 0) n = 1;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess || n <= 0) return 0;
     cache[dev].store(n, std::memory_order_relaxed);
     return n;
 }
