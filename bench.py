@@ -44,15 +44,24 @@ def parse():
     ap.add_argument("--warmup", type=int, default=100,
                     help="untimed steps before each timed loop (eager and graph): the GPU clock "
                          "rises over the first ~20 ms of sustained work")
-    ap.add_argument("--config", default="c2", help="workload: c1..c5 (default c2, Qwen3-shaped)")
+    ap.add_argument("--config", default="c5",
+                    help="workload: c1..c5 (default c5, the DeepSeek-V3-shaped layer, the largest)")
     ap.add_argument("--placement", default="coact", choices=["coact", "seq"])
-    ap.add_argument("--p", type=float, default=0.3, help="pruning threshold (paper: 0.3 for Qwen3)")
+    ap.add_argument("--p", type=float, default=None,
+                    help="pruning threshold (default: the workload's; the paper uses 0.3 for Qwen3 "
+                         "and 0.1 for DeepSeek-V2-Lite)")
     ap.add_argument("--c", type=float, default=5.0, help="inter-node cost")
     ap.add_argument("--rank", type=int, default=0)
     ap.add_argument("--eager", action="store_true",
                     help="time eager launches (default: the step captured once as a HIP graph, replayed)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-stride", type=int, default=4, help="oracle FFN runs every n-th rank-0 row")
+    ap.add_argument("--quick", action="store_true",
+                    help="only the timed step and its FFN timing (no stage times, cold-cache replays, "
+                         "sweeps, spectrum, second workload): for profiler runs")
+    ap.add_argument("--aux-config", default="c2",
+                    help="second workload measured briefly into aux (graph-replayed step and FFN); "
+                         "'none' to skip")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -269,6 +278,99 @@ def cpu_model():
     return "unknown"
 
 
+# Pruning threshold of each workload when --p is not given: the paper's 0.3
+# for the Qwen3-shaped layers and 0.1 for the DeepSeek-shaped ones
+# (Sec. VIII-A); the 16-rank layer is swept, 0.1 is its middle point.
+DEFAULT_P = {"c1": 0.3, "c1u": 0.3, "c2": 0.3, "c3": 0.1, "c4": 0.1, "c5": 0.1}
+
+
+def build_layer(cfg, placement_kind, p, c, rank):
+    """Inputs, placement, weights and buffers of one workload, resident in HBM;
+    the front end has run once and the rows other ranks return are seeded
+    stand-in values."""
+    import numpy as np
+    import torch
+    from paper_2607_05116_amd.layer import DeviceLayer
+    from workloads import generator as gen
+    t_setup = time.perf_counter()
+    logits = gen.logits(cfg)
+    x = gen.activations(cfg)
+    coact_counts = None
+    if placement_kind == "coact":
+        er, el, coact_counts = product_placement(cfg, p, c)
+    else:
+        er, el = gen.sequential_placement(cfg)
+    L = DeviceLayer(cfg, logits, x, er, el, p, c)
+    L.set_rank_weights(rank, *rank_weights(gen, cfg, er, el, rank))
+    if cfg.n_shared:
+        L.set_shared_weights(*gen.shared_weights(cfg))
+    L.front()
+    torch.cuda.synchronize()
+    n_recv = int(L.host("recv_offsets")[-1])
+    g = torch.Generator(device="cuda").manual_seed(1234)
+    L.parts[:n_recv] = (torch.randn((n_recv, cfg.d), generator=g, device="cuda") * 0.05).to(L.tdt)
+    log(f"{cfg.name}: setup {time.perf_counter() - t_setup:.1f} s; rank-{rank} rows {L.rank_rows(rank)}, "
+        f"received rows {n_recv}")
+    return L, logits, x, er, el, coact_counts
+
+
+def check_ffn_waits(L):
+    """The fused FFN's bounded cross-workgroup waits never gave up (the
+    counter the layer passes to every FFN call)."""
+    n = L.ffn_wait_errors()
+    if n:
+        raise RuntimeError(f"fused FFN: {n} cross-workgroup waits gave up (results of those calls are invalid)")
+    return n
+
+
+def time_graph(graph, stream, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    g0.record(stream)
+    for _ in range(steps):
+        graph.replay()
+    g1.record(stream)
+    torch.cuda.synchronize()
+    return g0.elapsed_time(g1) / steps, time.perf_counter() - wall0
+
+
+def aux_workload(name, rank, steps, warmup, c):
+    """A second workload measured briefly: its graph-replayed step and the
+    FFN call inside it (HIP events on the FFN's stream)."""
+    import torch
+    from workloads import generator as gen
+    cfg = gen.CONFIGS[name]
+    p = DEFAULT_P[name]
+    L, *_ = build_layer(cfg, "coact", p, c, rank)
+    stream = torch.cuda.current_stream()
+    side = torch.cuda.Stream() if cfg.n_shared else None
+    graph = L.capture_step(rank, side=side)
+    for _ in range(warmup):
+        L.step(rank, side=side)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        L.step(rank, side=side, ffn_events=ev[i])
+    torch.cuda.synchronize()
+    ffn_ms = sum(a.elapsed_time(b) for a, b in ev) / steps
+    ms, _ = time_graph(graph, stream, steps, warmup)
+    check_ffn_waits(L)
+    rows = L.rank_rows(rank)
+    flops = 6.0 * cfg.d * cfg.inter * rows
+    out = {"workload": f"{name}: T={cfg.T}, d={cfg.d}, E={cfg.E} top-{cfg.k}, inter={cfg.inter}, R={cfg.R}, "
+                       f"coact placement, p={p:g}, rank {rank}",
+           "ms_per_step": ms, "tokens_per_s": cfg.tokens_per_rank / (ms * 1e-3),
+           "ffn_ms": ffn_ms, "ffn_rows": rows, "ffn_tflops": flops / (ffn_ms * 1e-3) / 1e12,
+           "ffn_frac_bf16_peak": flops / (ffn_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS}
+    del graph, L
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -284,30 +386,15 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2607_05116_amd.layer import DeviceLayer
     from workloads import generator as gen
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     cfg = gen.CONFIGS[args.config]
+    if args.p is None:
+        args.p = DEFAULT_P[args.config]
     rank = args.rank
-    t_setup = time.perf_counter()
-    logits = gen.logits(cfg)
-    x = gen.activations(cfg)
-    if args.placement == "coact":
-        er, el, coact_counts = product_placement(cfg, args.p, args.c)
-    else:
-        er, el = gen.sequential_placement(cfg)
-    L = DeviceLayer(cfg, logits, x, er, el, args.p, args.c)
-    L.set_rank_weights(rank, *rank_weights(gen, cfg, er, el, rank))
-    if cfg.n_shared:
-        L.set_shared_weights(*gen.shared_weights(cfg))
-    L.front()
-    torch.cuda.synchronize()
-    n_recv = int(L.host("recv_offsets")[-1])
-    g = torch.Generator(device="cuda").manual_seed(1234)
-    L.parts[:n_recv] = (torch.randn((n_recv, cfg.d), generator=g, device="cuda") * 0.05).to(L.tdt)
-    log(f"setup {time.perf_counter() - t_setup:.1f} s; rank-{rank} rows {L.rank_rows(rank)}, received rows {n_recv}")
+    L, logits, x, er, el, coact_counts = build_layer(cfg, args.placement, args.p, args.c, rank)
 
     stream = torch.cuda.current_stream()
     # a side stream for the shared experts and the co-activation counts when
@@ -346,20 +433,11 @@ def main():
     graph_ms_per_step = cold_ms_per_step = cold_dirty_ms_per_step = composite = None
     if graph is not None:
         # the same step captured once as a HIP graph and replayed K times
-        for _ in range(args.warmup):
-            graph.replay()
-        torch.cuda.synchronize()
-        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        wall0 = time.perf_counter()
-        g0.record(stream)
-        for _ in range(K):
-            graph.replay()
-        g1.record(stream)
-        torch.cuda.synchronize()
-        wall = time.perf_counter() - wall0
-        graph_ms_per_step = g0.elapsed_time(g1) / K
+        graph_ms_per_step, wall = time_graph(graph, stream, K, args.warmup)
         ms_per_step = graph_ms_per_step
         log(f"graph replays: {graph_ms_per_step:.4f} ms/step (host wall {1e3 * wall / K:.4f} ms/step)")
+    check_ffn_waits(L)
+    if graph is not None and not args.quick:
         # the same replays with the caches cold: 512 MB (twice the 256 MB
         # Infinity Cache) read before each, outside its timed window, which
         # leaves the caches full of clean lines of other data; and the same
@@ -393,15 +471,7 @@ def main():
         fg = torch.cuda.CUDAGraph()
         with torch.cuda.graph(fg):
             L.front(side=side)
-        for _ in range(args.warmup):
-            fg.replay()
-        f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        f0.record(stream)
-        for _ in range(K):
-            fg.replay()
-        f1.record(stream)
-        torch.cuda.synchronize()
-        front_ms = f0.elapsed_time(f1) / K
+        front_ms, _ = time_graph(fg, stream, K, args.warmup)
         composite = {
             "front_graph_ms": front_ms,
             "rank0_step_ms": graph_ms_per_step - front_ms * (1.0 - 1.0 / cfg.R),
@@ -411,6 +481,83 @@ def main():
         }
         log(f"front end alone: {front_ms:.4f} ms; composite rank-0 rate {composite['tokens_per_s'] / 1e6:.2f} M tokens/s")
 
+    rows = L.rank_rows(rank)
+    flops = 6.0 * cfg.d * cfg.inter * rows
+    achieved = flops / (ffn_ms * 1e-3) / 1e12
+    workload_key = f"{cfg.name}_{args.placement}_p{args.p:g}"
+    traffic = traffic_from_profile(workload_key)
+    totals = L.host("totals").astype(np.int64)
+    eb = cfg.elem_bytes
+    send_copies = int(totals[1] + totals[2])
+    loads = np.diff(L.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
+    result = {
+        "metric": METRIC,
+        "value": cfg.tokens_per_rank / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded latent-topic router logits, N(0,1) activations, scaled random-init weights)",
+        "config": {
+            "workload": (f"{cfg.name}: MoE layer T={cfg.T} tokens ({cfg.R} virtual ranks x {cfg.tokens_per_rank}), "
+                         f"d={cfg.d}, E={cfg.E} top-{cfg.k}, SwiGLU inter={cfg.inter}"
+                         + (f" + {cfg.n_shared} shared x {cfg.shared_inter}" if cfg.n_shared else "")
+                         + f", {args.placement} placement, p={args.p:g}, c={args.c:g}, FFN/combine on rank {rank}"),
+            "name": cfg.name,
+            "T": cfg.T, "tokens_per_rank": cfg.tokens_per_rank, "d": cfg.d, "E": cfg.E, "k": cfg.k,
+            "inter": cfg.inter, "R": cfg.R, "ranks_per_node": cfg.ranks_per_node,
+            "n_shared": cfg.n_shared, "shared_inter": cfg.shared_inter,
+            "placement": args.placement, "p": args.p, "c": args.c, "rank": rank,
+            "parallelism": "1 GPU, virtual EP ranks",
+        },
+        "roofline": {
+            "kernel": ("cap_expert_ffn_gather, rank 0: one fused gate/up + down launch reading x rows in place "
+                       "(the call's events also hold its one-block counter clear, a few us)"),
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+            "flops_per_call": flops, "rows": rows, "avg_call_ms": ffn_ms,
+        },
+        "aux": {
+            "send_bytes_per_token": send_copies * cfg.d * eb / cfg.T,
+            "send_bytes_per_token_intra": int(totals[1]) * cfg.d * eb / cfg.T,
+            "send_bytes_per_token_inter": int(totals[2]) * cfg.d * eb / cfg.T,
+            "device_per_token": int(totals[0]) / cfg.T,
+            "node_per_token": int(totals[3]) / cfg.T,
+            "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
+            "rank_rows": rows,
+            "host_wall_ms_per_step": 1e3 * wall / K,
+            "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
+            "cold_cache_ms_per_step": cold_ms_per_step,
+            "cold_cache_dirty_ms_per_step": cold_dirty_ms_per_step,
+            "composite_rank0": composite,
+            "ffn_wait_errors": 0,
+        },
+    }
+    if not args.quick:
+        result["aux"].update(detail_measurements(args, L, cfg, rank, stream, coact_counts, er, el, totals))
+    if not args.no_cpu:
+        log("timing the CPU oracle on a bounded sample ...")
+        result["cpu_baseline"] = cpu_baseline(cfg, args.p, args.c, logits, x, args.cpu_stride)
+    if not args.quick and args.aux_config not in ("none", "", args.config):
+        del graph, L
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        log(f"second workload {args.aux_config} ...")
+        result["aux"]["second_workload"] = aux_workload(args.aux_config, rank, K, args.warmup, args.c)
+    print(json.dumps(result), flush=True)
+
+
+def detail_measurements(args, L, cfg, rank, stream, coact_counts, er, el, totals):
+    """Untimed detail of the headline workload: per-stage device times and
+    HBM rates, CAP against expert-level pruning, the pruning sweep, the
+    placement spectrum and the fused router front end."""
+    import numpy as np
+    import torch
     # per-stage device times (separate, untimed): each stage captured as a graph
     # of 20 back-to-back calls (every stage rewrites the same buffers from
     # unchanged inputs) and replayed, so launch gaps do not enter the times
@@ -445,16 +592,10 @@ def main():
             stage_ms[s_name] = 0.0
             continue
         stage_ms[s_name] = round(stage_time(fn), 5)
+    check_ffn_waits(L)
 
     rows = L.rank_rows(rank)
-    flops = 6.0 * cfg.d * cfg.inter * rows
-    achieved = flops / (ffn_ms * 1e-3) / 1e12
-    workload_key = f"{cfg.name}_{args.placement}_p{args.p:g}"
-    traffic = traffic_from_profile(workload_key)
-    totals = L.host("totals").astype(np.int64)
     eb = cfg.elem_bytes
-    send_copies = int(totals[1] + totals[2])
-    loads = np.diff(L.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
     # HBM roofline context for the row movers (algorithmic bytes / measured time)
     U = int(L.host("recv_offsets")[rank + 1] - L.host("recv_offsets")[rank])
     mask = L.host("mask").view(np.uint64)[rank * cfg.tokens_per_rank:(rank + 1) * cfg.tokens_per_rank]
@@ -509,61 +650,9 @@ def main():
         log(f"placement spectrum: {spectrum['total_swaps']} swaps, {time.perf_counter() - t_spec:.1f} s")
 
     front_end = fused_front_end(L, cfg, stream)
-
-    result = {
-        "metric": METRIC,
-        "value": cfg.tokens_per_rank / (ms_per_step * 1e-3),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": cfg.dtype,
-        "data": "synthetic (seeded latent-topic router logits, N(0,1) activations, scaled random-init weights)",
-        "config": {
-            "workload": (f"{cfg.name}: MoE layer T={cfg.T} tokens ({cfg.R} virtual ranks x {cfg.tokens_per_rank}), "
-                         f"d={cfg.d}, E={cfg.E} top-{cfg.k}, SwiGLU inter={cfg.inter}"
-                         + (f" + {cfg.n_shared} shared x {cfg.shared_inter}" if cfg.n_shared else "")
-                         + f", {args.placement} placement, p={args.p:g}, c={args.c:g}, FFN/combine on rank {rank}"),
-            "T": cfg.T, "tokens_per_rank": cfg.tokens_per_rank, "d": cfg.d, "E": cfg.E, "k": cfg.k,
-            "inter": cfg.inter, "R": cfg.R, "ranks_per_node": cfg.ranks_per_node,
-            "placement": args.placement, "p": args.p, "c": args.c, "rank": rank,
-            "parallelism": "1 GPU, virtual EP ranks",
-        },
-        "roofline": {
-            "kernel": "cap_expert_ffn_gather (one fused gate/up + down launch reading x rows in place), rank 0",
-            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
-            "flops_per_call": flops, "rows": rows, "avg_call_ms": ffn_ms,
-        },
-        "aux": {
-            "stage_ms": stage_ms,
-            "stage_hbm_GBs": hbm,
-            "send_bytes_per_token": send_copies * cfg.d * eb / cfg.T,
-            "send_bytes_per_token_intra": int(totals[1]) * cfg.d * eb / cfg.T,
-            "send_bytes_per_token_inter": int(totals[2]) * cfg.d * eb / cfg.T,
-            "device_per_token": int(totals[0]) / cfg.T,
-            "node_per_token": int(totals[3]) / cfg.T,
-            "load_imbalance_max_over_mean": float(loads.max() / loads.mean()),
-            "pruning_cap_vs_naive": pruning,
-            "pruning_sweep": sweep,
-            "placement_spectrum": spectrum,
-            "fused_router_front_end": front_end,
-            "rank_rows": rows, "rank_received_tokens": U,
-            "host_wall_ms_per_step": 1e3 * wall / K,
-            "eager_ms_per_step": eager_ms_per_step, "graph_ms_per_step": graph_ms_per_step,
-            "cold_cache_ms_per_step": cold_ms_per_step,
-            "cold_cache_dirty_ms_per_step": cold_dirty_ms_per_step,
-            "composite_rank0": composite,
-        },
-    }
-    if not args.no_cpu:
-        log("timing the CPU oracle on a bounded sample ...")
-        result["cpu_baseline"] = cpu_baseline(cfg, args.p, args.c, logits, x, args.cpu_stride)
-    print(json.dumps(result), flush=True)
+    return {"stage_ms": stage_ms, "stage_hbm_GBs": hbm, "pruning_cap_vs_naive": pruning,
+            "pruning_sweep": sweep, "placement_spectrum": spectrum, "fused_router_front_end": front_end,
+            "rank_received_tokens": U}
 
 
 if __name__ == "__main__":

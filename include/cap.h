@@ -226,7 +226,11 @@ cap_status cap_dispatch_layout(const cap_topology *topo, const int32_t *idx, con
                                void *ws, size_t ws_bytes, void *stream);
 
 /*
- * Token permutation, rows of d values of `dtype` (d % 8 == 0 for bf16, % 4 for f32).
+ * Token permutation (Sec. II-B: a rank dispatches each token's hidden state
+ * to the ranks of its selected experts and the receiver expands it into the
+ * rows of each local expert; Sec. II-C: one copy per destination device, so
+ * that device's experts share it), rows of d values of `dtype` (d % 8 == 0
+ * for bf16, % 4 for f32).
  *   CAP_PERMUTE_EXPERT_GATHER, rank r: out[slot_pos(t,s) - expert_offsets[r*E_loc]]
  *       = x[t] for every kept slot on r.  out holds rank r's expert-sorted rows.
  *   CAP_PERMUTE_SEND_PACK, rank s: out[send_offsets[s][d] + j] = x[t] for the
@@ -268,9 +272,9 @@ cap_status cap_permute(const cap_topology *topo, cap_permute_mode mode, int32_t 
  * bf16 calls with max_rows >= 8192 run both GEMMs in one kernel with a tile
  * queue per XCD (a down tile starts once the gate/up tiles of its rows are
  * done) on a device of 8 XCDs (or one); other calls run one kernel per GEMM.
- * Both give the same bits.
- * The environment variable CAP_FFN_FUSED_GRID=n caps the fused kernel's grid
- * at n workgroups (for tests; the result does not change).
+ * Both give the same bits.  The fused kernel's waits between workgroups are
+ * bounded; one that gives up leaves that call's output invalid and is counted
+ * only where cap_expert_ffn_ex is given a counter (cap_ffn_options).
  */
 cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter,
                           int32_t max_rows, const void *xs, const int32_t *row_offsets,
@@ -296,6 +300,42 @@ cap_status cap_expert_ffn_gather(cap_dtype dtype, int32_t E_loc, int32_t d, int3
                                  const int32_t *row_src, const int32_t *row_offsets,
                                  const void *w1, const void *w3, const void *w2, void *y,
                                  void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Options of cap_expert_ffn_ex (all fields 0 / NULL: the behaviour of
+ * cap_expert_ffn and cap_expert_ffn_gather).
+ *   wait_errors         (device int32, nullable) the fused kernel adds 1 for
+ *                       every wait between workgroups that gave up after
+ *                       spin_limit polls; the output of such a call is invalid.
+ *                       Never reset by the library: the caller zeroes it and
+ *                       reads it after synchronising.
+ *   max_workgroups      > 0 caps the fused kernel's grid (tests: with fewer
+ *                       workgroups than XCDs the last one runs the queues no
+ *                       workgroup touched; the result does not change).
+ *   spin_limit          > 0 replaces the default of 2^20 polls per wait.
+ *   force_wait_timeout  != 0 (tests of the give-up path only) makes every
+ *                       wait's target unreachable: each down tile waits once
+ *                       and gives up after spin_limit polls, every kernel
+ *                       still finishes, the output is invalid and
+ *                       *wait_errors grows by the number of down tiles.
+ */
+typedef struct {
+    int32_t *wait_errors;
+    int32_t max_workgroups;
+    int32_t spin_limit;
+    int32_t force_wait_timeout;
+} cap_ffn_options;
+
+/*
+ * cap_expert_ffn (row_src == NULL; x is then the expert-sorted xs and x_rows
+ * is ignored) or cap_expert_ffn_gather (row_src != NULL), with options (Eq. 1
+ * Expert_i; Sec. II-C expansion).  opt may be NULL.  Same arguments,
+ * arithmetic, workspace, limits and errors as those two calls.
+ */
+cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                             const void *x, int32_t x_rows, const int32_t *row_src, const int32_t *row_offsets,
+                             const void *w1, const void *w3, const void *w2, void *y, void *ws,
+                             size_t ws_bytes, const cap_ffn_options *opt, void *stream);
 
 /*
  * Weighted combine (Sec. II-C local aggregation and final combination; Eq. 1).

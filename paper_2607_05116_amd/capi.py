@@ -7,7 +7,7 @@ call raises CapError on a non-zero status.
 
 Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_router_route_prune,
 cap_dispatch_layout,
-cap_permute, cap_expert_ffn, cap_expert_ffn_gather, cap_combine, cap_coactivation,
+cap_permute, cap_expert_ffn, cap_expert_ffn_gather, cap_expert_ffn_ex, cap_combine, cap_coactivation,
 cap_workspace_size, cap_status_string, cap_version.
 """
 from __future__ import annotations
@@ -29,8 +29,8 @@ CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
            "cap_router_route_prune",
-           "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_combine",
-           "cap_coactivation"]
+           "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_expert_ffn_ex",
+           "cap_combine", "cap_coactivation"]
 
 
 class CapError(RuntimeError):
@@ -44,6 +44,11 @@ class Topology(ctypes.Structure):
                 ("T", ctypes.c_int32), ("tokens_per_rank", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("expert_rank", ctypes.c_void_p), ("expert_local", ctypes.c_void_p),
                 ("inter_node_cost", ctypes.c_float)]
+
+
+class FfnOptions(ctypes.Structure):
+    _fields_ = [("wait_errors", ctypes.c_void_p), ("max_workgroups", ctypes.c_int32),
+                ("spin_limit", ctypes.c_int32), ("force_wait_timeout", ctypes.c_int32)]
 
 
 class Layout(ctypes.Structure):
@@ -74,6 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                            ctypes.c_int),
         "cap_expert_ffn_gather": ([ctypes.c_int, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz,
                                    vp], ctypes.c_int),
+        "cap_expert_ffn_ex": ([ctypes.c_int, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz,
+                               P(FfnOptions), vp], ctypes.c_int),
         "cap_combine": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, i32, vp, vp, vp, vp,
                          P(Layout), vp, vp, i32, vp], ctypes.c_int),
         "cap_coactivation": ([i32, i32, i32, vp, vp, vp, i32, vp, sz, vp], ctypes.c_int),
@@ -179,6 +186,20 @@ def cap_expert_ffn_gather(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, 
     _check("cap_expert_ffn_gather", _lib.cap_expert_ffn_gather(
         dtype, E_loc, d, inter, max_rows, _ptr(x), int(x_rows), _ptr(row_src), _ptr(row_offsets), _ptr(w1),
         _ptr(w3), _ptr(w2), _ptr(y), _ptr(ws), nbytes, _stream(stream)))
+
+
+def make_ffn_options(wait_errors=None, max_workgroups=0, spin_limit=0, force_wait_timeout=False) -> FfnOptions:
+    """wait_errors: an int32 device tensor the fused kernel adds its given-up waits to."""
+    return FfnOptions(_ptr(wait_errors), int(max_workgroups), int(spin_limit), int(bool(force_wait_timeout)))
+
+
+def cap_expert_ffn_ex(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2, y, ws,
+                      ws_bytes=None, options: FfnOptions | None = None, stream=None):
+    nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
+    _check("cap_expert_ffn_ex", _lib.cap_expert_ffn_ex(
+        dtype, E_loc, d, inter, max_rows, _ptr(x), int(x_rows), _ptr(row_src), _ptr(row_offsets), _ptr(w1),
+        _ptr(w3), _ptr(w2), _ptr(y), _ptr(ws), nbytes, ctypes.byref(options) if options is not None else None,
+        _stream(stream)))
 
 
 def cap_combine(topo, mode, rank, dtype, d, inp, in_rows, idx, w, keep, dst_mask, layout: Layout,

@@ -23,7 +23,8 @@ cap_status combine_launch(const cap_topology*, cap_combine_mode, int, cap_dtype,
 size_t ffn_workspace_bytes(int, int, cap_dtype);
 cap_status ffn_supported(cap_dtype, int, int);
 cap_status expert_ffn_launch(cap_dtype, int, int, int, int, const void*, int, const int32_t*, const int32_t*,
-                             const void*, const void*, const void*, void*, void*, hipStream_t);
+                             const void*, const void*, const void*, void*, void*, const cap_ffn_options*,
+                             hipStream_t);
 size_t coact_workspace_bytes(int, int);
 cap_status coactivation_launch(int, int, int, const int32_t*, const uint8_t*, uint32_t*, int, void*,
                                hipStream_t);
@@ -173,41 +174,47 @@ cap_status cap_permute(const cap_topology* topo, cap_permute_mode mode, int32_t 
                           as_stream(stream));
 }
 
-cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
-                          const void* xs, const int32_t* row_offsets, const void* w1, const void* w3, const void* w2,
-                          void* y, void* ws, size_t ws_bytes, void* stream) {
-    if (!xs || !row_offsets || !w1 || !w3 || !w2 || !y) return CAP_ERR_INVALID_ARG;
+cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                             const void* x, int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets,
+                             const void* w1, const void* w3, const void* w2, void* y, void* ws, size_t ws_bytes,
+                             const cap_ffn_options* opt, void* stream) {
+    if (!x || !row_offsets || !w1 || !w3 || !w2 || !y) return CAP_ERR_INVALID_ARG;
     if (E_loc < 1 || E_loc > kMaxE || d < 1 || inter < 1 || max_rows < 0) return CAP_ERR_INVALID_ARG;
+    if (row_src && x_rows < 1) return CAP_ERR_INVALID_ARG;
+    if (opt && (opt->max_workgroups < 0 || opt->spin_limit < 0)) return CAP_ERR_INVALID_ARG;
+    if (opt && opt->wait_errors && (reinterpret_cast<uintptr_t>(opt->wait_errors) & 3) != 0)
+        return CAP_ERR_INVALID_ARG;
     if (dtype != CAP_DTYPE_BF16 && dtype != CAP_DTYPE_F32) return CAP_ERR_UNSUPPORTED;
     const cap_status sup = ffn_supported(dtype, d, inter);
     if (sup != CAP_OK) return sup;
-    if (!aligned16(xs) || !aligned16(y) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2))
+    if (row_src) {
+        // gathered row offsets are 32-bit byte offsets from x
+        const unsigned long long x_bytes =
+            static_cast<unsigned long long>(x_rows) * d * (dtype == CAP_DTYPE_BF16 ? 2u : 4u);
+        if (x_bytes >= (1ull << 32)) return CAP_ERR_UNSUPPORTED;
+    }
+    if (!aligned16(x) || !aligned16(y) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2))
         return CAP_ERR_INVALID_ARG;
     if (!ws || ws_bytes < ffn_workspace_bytes(max_rows, inter, dtype) || !aligned16(ws)) return CAP_ERR_WORKSPACE;
     if (max_rows == 0) return CAP_OK;
-    return expert_ffn_launch(dtype, E_loc, d, inter, max_rows, xs, 0, nullptr, row_offsets, w1, w3, w2, y, ws,
-                             as_stream(stream));
+    return expert_ffn_launch(dtype, E_loc, d, inter, max_rows, x, row_src ? x_rows : 0, row_src, row_offsets, w1,
+                             w3, w2, y, ws, opt, as_stream(stream));
+}
+
+cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                          const void* xs, const int32_t* row_offsets, const void* w1, const void* w3, const void* w2,
+                          void* y, void* ws, size_t ws_bytes, void* stream) {
+    return cap_expert_ffn_ex(dtype, E_loc, d, inter, max_rows, xs, 0, nullptr, row_offsets, w1, w3, w2, y, ws,
+                             ws_bytes, nullptr, stream);
 }
 
 cap_status cap_expert_ffn_gather(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
                                  const void* x, int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets,
                                  const void* w1, const void* w3, const void* w2, void* y, void* ws,
                                  size_t ws_bytes, void* stream) {
-    if (!x || !row_src || !row_offsets || !w1 || !w3 || !w2 || !y) return CAP_ERR_INVALID_ARG;
-    if (E_loc < 1 || E_loc > kMaxE || d < 1 || inter < 1 || max_rows < 0 || x_rows < 1) return CAP_ERR_INVALID_ARG;
-    if (dtype != CAP_DTYPE_BF16 && dtype != CAP_DTYPE_F32) return CAP_ERR_UNSUPPORTED;
-    const cap_status sup = ffn_supported(dtype, d, inter);
-    if (sup != CAP_OK) return sup;
-    // gathered row offsets are 32-bit byte offsets from x
-    const unsigned long long x_bytes =
-        static_cast<unsigned long long>(x_rows) * d * (dtype == CAP_DTYPE_BF16 ? 2u : 4u);
-    if (x_bytes >= (1ull << 32)) return CAP_ERR_UNSUPPORTED;
-    if (!aligned16(x) || !aligned16(y) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2))
-        return CAP_ERR_INVALID_ARG;
-    if (!ws || ws_bytes < ffn_workspace_bytes(max_rows, inter, dtype) || !aligned16(ws)) return CAP_ERR_WORKSPACE;
-    if (max_rows == 0) return CAP_OK;
-    return expert_ffn_launch(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2, y, ws,
-                             as_stream(stream));
+    if (!row_src) return CAP_ERR_INVALID_ARG;
+    return cap_expert_ffn_ex(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2, y, ws,
+                             ws_bytes, nullptr, stream);
 }
 
 cap_status cap_combine(const cap_topology* topo, cap_combine_mode mode, int32_t rank, cap_dtype dtype, int32_t d,

@@ -23,7 +23,6 @@
 // fp32 path: a plain LDS-tiled FMA kernel (small shapes only).
 #include "cap_device.hpp"
 
-#include <cstdlib>
 #include <type_traits>
 
 namespace cap {
@@ -529,20 +528,25 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
 // No wait can deadlock: a workgroup waits (before a down tile) only once every
 // gate/up tile of its XCD's queue has been claimed; a gate/up tile is claimed
 // only by a running workgroup and never waits, and a workgroup delivers its own
-// pending counts before it waits.  Each wait is also bounded (kSpinLimit
-// polls): past it the kernel adds 1 to the error word and goes on.  A queue no
-// workgroup touched (an XCD that ran none of them) is run by the last
-// workgroup to finish, so every tile is computed whatever the dispatch.
+// pending counts before it waits.  Each wait is also bounded (spin_limit
+// polls): past it the kernel adds 1 to *wait_err (the caller's counter, or a
+// word of the workspace when the caller passes none) and goes on, so a wait
+// that gave up is visible to the caller.  A queue no workgroup touched (an XCD
+// that ran none of them) is run by the last workgroup to finish, so every tile
+// is computed whatever the dispatch.  target_bias is 0; a caller testing the
+// give-up path passes 1, which makes every wait's target unreachable, so each
+// down tile waits once and gives up after spin_limit polls.
 //
 // sync (ints, zero at launch): the queue counter of XCD x at
-// x * kSyncQueueStride, the error word, the finished-workgroup count, then
-// one ready counter per m-tile.
+// x * kSyncQueueStride, the workspace error word, the finished-workgroup
+// count, then one ready counter per m-tile.
 constexpr int kSyncQueueStride = 32;                 // one 128-byte line per queue counter
 constexpr int kMaxXcc = 8;
 constexpr int kSyncErr = kMaxXcc * kSyncQueueStride;
 constexpr int kSyncDone = kSyncErr + 1;
 constexpr int kSyncReady = kSyncErr + kSyncQueueStride;
-constexpr int kSpinLimit = 1 << 20;
+constexpr int kGroupM = 4;                 // m-tiles per group of the queue order
+constexpr int kSpinLimit = 1 << 20;        // default polls before a wait gives up
 
 __device__ __forceinline__ int xcc_register() {
     int x;
@@ -559,7 +563,8 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W1, const uint16_t* __restrict__ W3,
     const uint16_t* __restrict__ W2, uint16_t* __restrict__ H, uint16_t* __restrict__ Y,
     const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int d, int inter,
-    const int32_t* __restrict__ row_src, int x_rows, int n_xcc, int* __restrict__ sync) {
+    const int32_t* __restrict__ row_src, int x_rows, int n_xcc, int* __restrict__ sync,
+    int* __restrict__ wait_err, int spin_limit, int target_bias) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
     __shared__ int row_begin[kMaxExpertsLocal];
@@ -571,7 +576,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
     build_schedule<kBM>(row_offsets, E_loc, max_rows, mt_prefix, row_begin, row_end);
     const int MT = mt_prefix[E_loc];
     const int n_gu = inter / (kBN / 2), n_dn = d / kBN;
-    const int target = n_gu * (kNW - kNL);
+    const int target = n_gu * (kNW - kNL) + target_bias;
     int* const ready = sync + kSyncReady;
     const int lane = threadIdx.x % kWave;
     const int wave = static_cast<int>(__builtin_amdgcn_readfirstlane(threadIdx.x / kWave));
@@ -580,16 +585,30 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
     const LaneMap lm = lane_map(lane);
 
-    // queue of XCD slot x: m-tiles [mb, me); gate/up entries [0, GU), down [GU, Q)
+    // queue of XCD slot x: m-tiles [mb, mb + MX); gate/up entries [0, GU), down [GU, Q)
     int x = xcc_register() % n_xcc;
-    int mb = 0, GU = 0, Q = 0;
+    int mb = 0, MX = 0, GU = 0, Q = 0;
     int* queue = sync;
     auto set_queue = [&](int xs) {
         mb = (xs * MT) / n_xcc;
-        const int me = ((xs + 1) * MT) / n_xcc;
-        GU = (me - mb) * n_gu;
-        Q = GU + (me - mb) * n_dn;
+        MX = ((xs + 1) * MT) / n_xcc - mb;
+        GU = MX * n_gu;
+        Q = GU + MX * n_dn;
         queue = sync + xs * kSyncQueueStride;
+    };
+    // Entry u of a GEMM with nn n-tiles -> (m-tile offset, n-tile): the m-tiles
+    // go in groups of kGroupM; within a group the n-tile is the outer index.
+    // The workgroups of an XCD then run a block of about kGroupM m-tiles x
+    // (CUs / kGroupM) n-tiles at a time, so each operand stream (an m-tile's
+    // rows, an n-tile's weight rows) is shared by several running tiles and
+    // the expert's weights are streamed into the XCD once per group of
+    // m-tiles instead of once per one or two m-tiles.
+    auto entry_tile = [&](int u, int nn, int& m_off, int& nt) {
+        const int g = u / (kGroupM * nn);
+        const int v = u - g * (kGroupM * nn);
+        const int gm = min(kGroupM, MX - g * kGroupM);
+        m_off = g * kGroupM + v % gm;
+        nt = v / gm;
     };
 
     struct Tile { int gu, m, nt, row0, rows, KT; };
@@ -601,9 +620,10 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
         Tile D;
         D.gu = t < GU ? 1 : 0;
         const int u = D.gu ? t : t - GU;
-        const int nn = D.gu ? n_gu : n_dn;
-        D.m = __builtin_amdgcn_readfirstlane(mb + u / nn);
-        D.nt = __builtin_amdgcn_readfirstlane(u % nn);
+        int m_off, nt;
+        entry_tile(u, D.gu ? n_gu : n_dn, m_off, nt);
+        D.m = __builtin_amdgcn_readfirstlane(mb + m_off);
+        D.nt = __builtin_amdgcn_readfirstlane(nt);
         D.KT = (D.gu ? d : inter) / kStageK;
         const int l = __builtin_amdgcn_readfirstlane(find_expert(mt_prefix, E_loc, D.m));
         D.row0 = __builtin_amdgcn_readfirstlane(row_begin[l] + (D.m - mt_prefix[l]) * kBM);
@@ -624,8 +644,8 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
         if (wave == 0 && lane == 0) {
             int polls = 0;
             while (atomic_add_agent(ready + m, 0) < target) {
-                if (++polls > kSpinLimit) {
-                    atomic_add_agent(sync + kSyncErr, 1);
+                if (++polls > spin_limit) {
+                    atomic_add_agent(wait_err, 1);
                     break;
                 }
                 __builtin_amdgcn_s_sleep(4);
@@ -685,7 +705,11 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
                     }
                     if (kt == KT - 2 && wave == 0) {
                         const int nx = bcast[0];
-                        if (nx >= GU && nx < Q && lane == 0) poll = atomic_add_agent(ready + mb + (nx - GU) / n_dn, 0);
+                        if (nx >= GU && nx < Q && lane == 0) {
+                            int m_off, nt;
+                            entry_tile(nx - GU, n_dn, m_off, nt);
+                            poll = atomic_add_agent(ready + mb + m_off, 0);
+                        }
                     }
                 }
                 const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
@@ -865,7 +889,7 @@ cap_status ffn_supported(cap_dtype dt, int d, int inter) {
 // xs[row_src[i]] and xs has x_rows rows.
 cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_rows, const void* xs, int x_rows,
                              const int32_t* row_src, const int32_t* row_offsets, const void* w1, const void* w3,
-                             const void* w2, void* y, void* ws, hipStream_t st) {
+                             const void* w2, void* y, void* ws, const cap_ffn_options* opt, hipStream_t st) {
     if (dt == CAP_DTYPE_BF16) {
         const auto* a = static_cast<const uint16_t*>(xs);
         const auto* b1 = static_cast<const uint16_t*>(w1);
@@ -882,18 +906,20 @@ cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_
             zero_ints_kernel<<<1, 256, 0, st>>>(sync, fused_sync_ints(max_rows));
             CAP_LAUNCH_CHECK();
             int g = persistent_grid(1ll << 30);
-            // CAP_FFN_FUSED_GRID=n caps the grid (testing: with fewer
-            // workgroups than XCDs the last one runs the untouched queues)
-            if (const char* e = std::getenv("CAP_FFN_FUSED_GRID")) {
-                const int v = std::atoi(e);
-                if (v > 0 && v < g) g = v;
-            }
+            // a caller's cap on the grid (with fewer workgroups than XCDs
+            // the last one runs the untouched queues)
+            if (opt && opt->max_workgroups > 0 && opt->max_workgroups < g) g = opt->max_workgroups;
+            int* err = (opt && opt->wait_errors) ? opt->wait_errors : sync + kSyncErr;
+            const int spin = (opt && opt->spin_limit > 0) ? opt->spin_limit : kSpinLimit;
+            const int bias = (opt && opt->force_wait_timeout) ? 1 : 0;
             if (row_src)
                 ffn_fused_bf16_kernel<true><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
-                                                                       max_rows, d, inter, row_src, x_rows, n_xcc, sync);
+                                                                       max_rows, d, inter, row_src, x_rows, n_xcc, sync,
+                                                                       err, spin, bias);
             else
                 ffn_fused_bf16_kernel<false><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
-                                                                        max_rows, d, inter, nullptr, 0, n_xcc, sync);
+                                                                        max_rows, d, inter, nullptr, 0, n_xcc, sync,
+                                                                        err, spin, bias);
             CAP_LAUNCH_CHECK();
             return CAP_OK;
         }

@@ -80,6 +80,9 @@ class DeviceLayer:
         self.y = torch.empty((cfg.tokens_per_rank, d), dtype=self.tdt, device=self.dev)
         self.ws_ffn = self._ws(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, cfg.inter,
                                                        self.row_cap, self.dt))
+        # waits of the fused FFN kernel that gave up (every FFN call adds to it)
+        self.ffn_err = torch.zeros(1, **i32)
+        self.ffn_opts = capi.make_ffn_options(self.ffn_err)
         self.weights: dict[int, tuple] = {}
         self.naive = False              # expert-level threshold pruning instead of CAP's
         self.fused_gather = True        # FFN reads x through row_src instead of a gathered copy
@@ -145,17 +148,17 @@ class DeviceLayer:
         w1, w3, w2 = self.weights[rank]
         E_loc = self.cfg.E_loc
         offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
-        capi.cap_expert_ffn(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.xs, offs,
-                            w1, w3, w2, self.Y, self.ws_ffn, stream=stream)
+        capi.cap_expert_ffn_ex(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.xs, 0, None, offs,
+                               w1, w3, w2, self.Y, self.ws_ffn, options=self.ffn_opts, stream=stream)
 
     def ffn_gather(self, rank: int, stream=None):
         """The rank's expert FFN reading its rows from x through row_src."""
         w1, w3, w2 = self.weights[rank]
         E_loc = self.cfg.E_loc
         offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
-        capi.cap_expert_ffn_gather(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.x,
-                                   self.x.shape[0], self.row_src, offs, w1, w3, w2, self.Y, self.ws_ffn,
-                                   stream=stream)
+        capi.cap_expert_ffn_ex(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.x,
+                               self.x.shape[0], self.row_src, offs, w1, w3, w2, self.Y, self.ws_ffn,
+                               options=self.ffn_opts, stream=stream)
 
     def shared_ffn(self, rank: int, stream=None):
         if self.shared is None:
@@ -163,8 +166,8 @@ class DeviceLayer:
         w1, w3, w2 = self.shared
         T_loc = self.cfg.tokens_per_rank
         xs = self.x[rank * T_loc:(rank + 1) * T_loc]
-        capi.cap_expert_ffn(self.dt, 1, self.d, w1.shape[0], T_loc, xs, self.shared_offsets,
-                            w1, w3, w2, self.shared_out, self.ws_shared, stream=stream)
+        capi.cap_expert_ffn_ex(self.dt, 1, self.d, w1.shape[0], T_loc, xs, 0, None, self.shared_offsets,
+                               w1, w3, w2, self.shared_out, self.ws_shared, options=self.ffn_opts, stream=stream)
 
     def dest_reduce(self, rank: int, stream=None):
         capi.cap_combine(self.topo, capi.CAP_COMBINE_DEST_REDUCE, rank, self.dt, self.d, self.Y,
@@ -262,6 +265,12 @@ class DeviceLayer:
         side_done.record(side)
         self.layout(main)
         self.rank_path(rank, main, ffn_events, join=side_done)
+
+    def ffn_wait_errors(self) -> int:
+        """Waits of the fused FFN kernel that gave up since the layer was made
+        (0 unless an FFN output is invalid).  Synchronises."""
+        torch.cuda.synchronize()
+        return int(self.ffn_err.item())
 
     # ------------------------------------------------------------ host views
     def host(self, name: str) -> np.ndarray:

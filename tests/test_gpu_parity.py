@@ -577,10 +577,11 @@ def test_ffn_fused_repeated_calls_identical():
 
 
 @pytest.mark.parametrize("grid", [1, 3])
-def test_ffn_fused_with_fewer_workgroups_than_xcds(grid, monkeypatch):
+def test_ffn_fused_with_fewer_workgroups_than_xcds(grid):
     """With the fused kernel's grid capped below the XCD count, the queues of
     XCDs that ran no workgroup are run by the last workgroup to finish: the
-    result is still complete and identical to the full grid's."""
+    result is still complete and identical to the full grid's, and no wait
+    gives up."""
     rng = np.random.default_rng(grid)
     d, inter, counts = 256, 128, [2000, 0, 3000, 1, 4000]
     E_loc, rows = len(counts), sum(counts)
@@ -594,18 +595,63 @@ def test_ffn_fused_with_fewer_workgroups_than_xcds(grid, monkeypatch):
     cdt = capi.CAP_DTYPE_BF16
     ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
                      dtype=torch.uint8, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
     outs = []
-    for cap in (None, grid):
-        if cap is None:
-            monkeypatch.delenv("CAP_FFN_FUSED_GRID", raising=False)
-        else:
-            monkeypatch.setenv("CAP_FFN_FUSED_GRID", str(cap))
+    for cap in (0, grid):
         y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
-        capi.cap_expert_ffn(cdt, E_loc, d, inter, max_rows, x, offs, w1, w3, w2, y, ws)
+        opts = capi.make_ffn_options(err, max_workgroups=cap)
+        capi.cap_expert_ffn_ex(cdt, E_loc, d, inter, max_rows, x, 0, None, offs, w1, w3, w2, y, ws, options=opts)
         torch.cuda.synchronize()
         outs.append(y[:rows].view(torch.int16).cpu().numpy())
-    monkeypatch.delenv("CAP_FFN_FUSED_GRID", raising=False)
+    assert int(err.item()) == 0
     assert np.array_equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("gathered", [False, True])
+def test_ffn_fused_wait_give_up_is_counted(gathered):
+    """The fused kernel's bounded waits report giving up.  The host makes every
+    wait's target unreachable with a spin limit of 1 poll: each of the
+    m-tiles x (d / 256) down tiles waits once and gives up, every kernel
+    finishes, and the caller's counter holds exactly that many.  A normal call
+    afterwards on the same workspace adds nothing and matches the two-kernel
+    path's bits."""
+    rng = np.random.default_rng(7)
+    d, inter, counts = 512, 256, [3000, 4000, 700]
+    E_loc, rows = len(counts), sum(counts)
+    max_rows = FUSED_MIN_ROWS + 108
+    assert rows < FUSED_MIN_ROWS <= max_rows
+    m_tiles = sum((c + 255) // 256 for c in counts)
+    offs = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)).cuda()
+    bf = lambda a: torch.from_numpy(a.astype(np.float32)).to(torch.bfloat16).cuda()
+    w1 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w3 = bf(rng.standard_normal((E_loc, inter, d)) / np.sqrt(d))
+    w2 = bf(rng.standard_normal((E_loc, d, inter)) / (12 * np.sqrt(inter)))
+    x = bf(rng.standard_normal((max_rows + 50, d)))
+    src = torch.from_numpy(rng.permutation(max_rows + 50)[:max_rows].astype(np.int32)).cuda()
+    cdt = capi.CAP_DTYPE_BF16
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_EXPERT_FFN, None, d, inter, max_rows, cdt),
+                     dtype=torch.uint8, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    y = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+
+    def call(opts, cap_rows=max_rows, out=y):
+        if gathered:
+            capi.cap_expert_ffn_ex(cdt, E_loc, d, inter, cap_rows, x, x.shape[0], src, offs, w1, w3, w2, out, ws,
+                                   options=opts)
+        else:
+            capi.cap_expert_ffn_ex(cdt, E_loc, d, inter, cap_rows, x, 0, None, offs, w1, w3, w2, out, ws,
+                                   options=opts)
+        torch.cuda.synchronize()
+
+    call(capi.make_ffn_options(err, spin_limit=1, force_wait_timeout=True))
+    assert int(err.item()) == m_tiles * (d // 256)
+    err.zero_()
+    call(capi.make_ffn_options(err))
+    assert int(err.item()) == 0
+    # the two-kernel path (capacity below the fused threshold) on the same rows
+    y2 = torch.zeros((max_rows, d), dtype=torch.bfloat16, device="cuda")
+    call(None, cap_rows=rows, out=y2)
+    assert torch.equal(y[:rows].view(torch.int16), y2[:rows].view(torch.int16))
 
 
 def test_ffn_f32_ragged_experts():

@@ -160,6 +160,24 @@ def test_send_pack_rows(orc):
         assert row == out.shape[0]
 
 
+def test_send_pack_matches_receive_buffers(orc):
+    """Independent of the send-pack enumeration: the rows source s sends to
+    device d are the rows of d's receive buffer that come from s, in the
+    buffer's order (recv_token of the layout, Sec. II-C one copy per device)."""
+    for cfgname, p, placement in [("c1", 0.3, "scrambled"), ("c1u", 0.0, "seq")]:
+        cfg, er, el, r, lay, x, wts = _tiny(orc, cfgname, p, placement)
+        T_loc = cfg.tokens_per_rank
+        for s in range(cfg.R):
+            out = orc.send_pack(x, r["mask"], lay["send_offsets"], lay["send_counts"], cfg.R, T_loc, s)
+            for dd in range(cfg.R):
+                a, b = lay["recv_offsets"][dd], lay["recv_offsets"][dd + 1]
+                toks = lay["recv_token"][a:b]
+                mine = toks[(toks >= s * T_loc) & (toks < (s + 1) * T_loc)]
+                o = int(np.asarray(lay["send_offsets"]).reshape(cfg.R, cfg.R)[s, dd])
+                assert len(mine) == int(np.asarray(lay["send_counts"]).reshape(cfg.R, cfg.R)[s, dd])
+                assert np.array_equal(out[o:o + len(mine)], x[mine])
+
+
 # ---------------------------------------------------------------- placement (Algorithm 1 + node stage)
 def _hub_block_counts(n, groups):
     """Co-activation counts with one hub per group: the hub co-activates more

@@ -105,6 +105,37 @@ def test_gates_closed_forms(orc):
     assert orc.gates(L, orc.topk(L, 1)).tolist() == [[1.0]]
 
 
+def test_gates_large_logit_gaps(orc):
+    """Gaps to the top logit far beyond the fp32 range of exp: the gates stay
+    finite.  A slot whose gap is at or above -87.33 gets exp(gap) / S (fp64
+    reference, S within one ulp of 1 here), one below the cutoff gets exactly 0
+    (the specified exponential never returns a subnormal), and the top slot
+    takes the rest."""
+    gaps = [0.0, -20.0, -80.0, -86.0, -87.33, -87.34, -88.0, -90.0, -150.0, -1e4]
+    base = np.float32(3.5)
+    L = (base + np.array([gaps], np.float32)).astype(np.float32)
+    real_gaps = (L[0].astype(np.float64) - float(L[0, 0]))
+    k = len(gaps)
+    w = orc.gates(L, orc.topk(L, k))[0]
+    assert np.all(np.isfinite(w))
+    assert w[0] == 1.0
+    for s in range(1, k):
+        g = np.float32(L[0, s] - L[0, 0])
+        if g >= np.float32(-87.33):
+            ref = math.exp(float(real_gaps[s]))
+            assert abs(float(w[s]) - ref) <= 2 * ref * 2.0 ** -23, (s, w[s], ref)
+            assert w[s] >= np.finfo(np.float32).tiny
+        else:
+            assert w[s] == 0.0, (s, w[s])
+    # the same gaps from the bottom of the fp32 range and from a large positive
+    # top logit (the shift is by the top logit, so nothing overflows)
+    for top in (np.float32(-3e4), np.float32(3e4)):
+        L2 = (top + np.array([[0.0, -10.0, -1e4]], np.float32)).astype(np.float32)
+        w2 = orc.gates(L2, orc.topk(L2, 3))[0]
+        assert np.all(np.isfinite(w2)) and w2[2] == 0.0
+        assert abs(float(w2.sum()) - 1.0) <= 3 * 2.0 ** -23
+
+
 # ---------------------------------------------------------------- pruning: hand-worked cases
 def _prune1(orc, experts, w, expert_rank, rpn, tpr, c, p, t=0):
     """Prune a single token t whose slots are `experts` with gates `w`."""
@@ -262,6 +293,62 @@ def test_naive_pruning_keeps_prefix(orc):
             for v in w[t, :n - 1]:
                 cum = np.float32(cum + v)
             assert cum < np.float32(0.7)
+
+
+def test_naive_pruning_mask_and_renormalised_gates(orc):
+    """Naive expert-level pruning (Sec. II-D; the baseline of Sec. VIII-D) on
+    random tokens: the device mask is the OR of the devices of the kept slots
+    only; kept gates are w / (sum of kept w) (fp64 reference, within the
+    rounding of an fp32 slot-order sum and one division), pruned slots are 0,
+    and the kept gates sum to 1."""
+    rng = np.random.default_rng(31)
+    L = gen.iid_logits(3000, 64, seed=13) * np.float32(2.5)
+    er = (rng.permutation(64) % 8).astype(np.int32)          # 8 experts per device, scrambled
+    for k, p in [(6, 0.3), (8, 0.1), (4, 0.5), (8, 0.45)]:
+        idx = orc.topk(L, k)
+        w = orc.gates(L, idx)
+        keep, wp, mask = orc.prune_naive(idx, w, er, p)
+        kept = keep == 1
+        assert kept[:, 0].all()
+        bits = np.where(kept, np.left_shift(np.uint64(1), er[idx].astype(np.uint64)), np.uint64(0))
+        assert np.array_equal(mask, np.bitwise_or.reduce(bits, axis=1))
+        assert np.all(wp[~kept] == 0)
+        S = np.where(kept, w.astype(np.float64), 0.0).sum(1)
+        ref = w.astype(np.float64) / S[:, None]
+        rel = np.abs(wp.astype(np.float64) - ref)[kept] / ref[kept]
+        assert rel.max() <= (k + 1) * 2.0 ** -24
+        assert np.abs(wp.astype(np.float64).sum(1) - 1).max() <= k * 2.0 ** -23
+        # some slot is pruned while its device stays kept (another kept slot
+        # shares it): the expert-level rule prunes slots, not devices
+        dev_kept = ((mask[:, None] >> er[idx].astype(np.uint64)) & np.uint64(1)) == 1
+        if p >= 0.3:
+            assert np.any(dev_kept & ~kept)
+
+
+def test_naive_pruning_hand_worked(orc):
+    """Hand-worked tokens of the expert-level rule.
+    Token 0: gates 0.5 / 0.3 / 0.2 on devices 0 / 1 / 2, p = 0.3: the running
+    sum 0.5 < 0.7, then 0.8 >= 0.7, so two slots stay, w' = 0.625 / 0.375 / 0
+    and the mask is {0, 1}.
+    Token 1: gates 0.5 / 0.25 / 0.25 on devices 1 / 0 / 1, p = 0.25: the sum
+    reaches 0.75 exactly at the second slot (exact in fp32), so the third slot
+    is pruned although its device 1 stays in the mask; w' = 2/3, 1/3, 0."""
+    er = np.array([0, 1, 2, 1, 3, 1], np.int32)
+    idx = np.array([[0, 1, 2]], np.int32)
+    w = np.array([[0.5, 0.3, 0.2]], np.float32)
+    keep, wp, mask = orc.prune_naive(idx, w, er, 0.3)
+    assert keep.tolist() == [[1, 1, 0]]
+    assert np.allclose(wp, [[0.625, 0.375, 0.0]], rtol=2 ** -23, atol=0)
+    assert int(mask[0]) == 0b011
+    idx = np.array([[3, 0, 5]], np.int32)
+    w = np.array([[0.5, 0.25, 0.25]], np.float32)
+    keep, wp, mask = orc.prune_naive(idx, w, er, 0.25)
+    assert keep.tolist() == [[1, 1, 0]]
+    assert np.allclose(wp, [[2 / 3, 1 / 3, 0.0]], rtol=2 ** -23, atol=0)
+    assert int(mask[0]) == 0b011
+    # p = 0 keeps every slot whatever the sum
+    keep, wp, mask = orc.prune_naive(idx, w, er, 0.0)
+    assert keep.tolist() == [[1, 1, 1]] and int(mask[0]) == 0b011
 
 
 def test_router_logits_definition(orc):
