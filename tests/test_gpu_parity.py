@@ -6,6 +6,7 @@ array, volumes, co-activation counts, permuted rows.  FFN and combine:
 normalised Frobenius error gate (1e-2 bf16, 1e-5 fp32).
 """
 import dataclasses
+import os
 
 import numpy as np
 import pytest
@@ -272,6 +273,83 @@ def test_route_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
     assert np.array_equal(Ld.host("coact").view(np.uint32), oracle.coactivation(r["idx"], r["keep"], E))
 
 
+def _edge_logits(T, E, k, seed):
+    """Rows whose gaps to the top logit span [-90, -80] (including exactly
+    -87.33 in fp32, the exponential's cutoff, and gaps whose 2^n scaling is
+    near the bottom of the normal range), with top logits 0 (so the gap is the
+    logit itself, exactly) or large."""
+    rng = np.random.default_rng(seed)
+    L = np.full((T, E), -1e4, np.float32)
+    edge = np.array([-80.0, -84.5, -86.0, -87.0, -87.33, -87.34, -88.0, -89.5, -90.0], np.float32)
+    for t in range(T):
+        top = np.float32(0.0) if t % 3 else np.float32(rng.uniform(-40, 40))
+        g = np.concatenate([[np.float32(0.0)], rng.permutation(edge)[:k - 1]]).astype(np.float32)
+        if t % 2:
+            g[1:] = g[1:] + rng.uniform(-0.5, 0.5, size=k - 1).astype(np.float32)
+        cols = rng.permutation(E)[:k]
+        L[t, cols] = (top + g).astype(np.float32) if top != 0 else g
+    return L
+
+
+def _exact_sum_logits(T, E, k, er, tokens_per_rank, rpn, seed):
+    """Tokens whose k selected logits are equal (gates exactly 1/k) and whose
+    experts sit two on one remote device and one on each of k - 2 other
+    remote devices of the same node: device scores 2/k, 1/k, ..., so the
+    greedy's fp32 running sum lands exactly on 1 - p for p = 1 - m/k."""
+    rng = np.random.default_rng(seed)
+    L = np.full((T, E), -5.0, np.float32)
+    R = int(er.max()) + 1
+    for t in range(T):
+        src = t // tokens_per_rank
+        node = src // rpn
+        others = [d for d in range(node * rpn, (node + 1) * rpn) if d != src]
+        devs = rng.permutation(others)[:k - 1]
+        chosen = []
+        for j, d in enumerate(devs):
+            pool = [e for e in np.flatnonzero(er == d) if e not in chosen]
+            take = 2 if j == 0 else 1
+            chosen += list(rng.choice(pool, size=take, replace=False))
+        L[t, chosen] = 5.0
+    return L
+
+
+@pytest.mark.parametrize("kind,p", [("cutoff", 0.3), ("cutoff", 0.0), ("exact", 0.25), ("exact", 0.5),
+                                    ("exact", 0.75)])
+def test_route_gate_cutoff_and_exact_greedy_sum(kind, p):
+    """Bit-exact routing where the arithmetic is at its edges: gate
+    exponentials around the -87.33 cutoff (returned as 0 below it, scaled by
+    2^n with n near -126 above it), and pruning whose fp32 running sum reaches
+    1 - p exactly (Eq. 6 keeps the device that makes it reach the target and
+    no more)."""
+    E, R, rpn = 64, 8, 8
+    k = 8 if kind == "cutoff" else 4
+    T = R * 96
+    perm = np.random.default_rng(5).permutation(E)
+    er, el = (perm // (E // R)).astype(np.int32), (perm % (E // R)).astype(np.int32)
+    if kind == "cutoff":
+        L = _edge_logits(T, E, k, 11)
+    else:
+        L = _exact_sum_logits(T, E, k, er, T // R, rpn, 12)
+    cfg = gen.Config("edge", T=T, d=8, E=E, k=k, inter=128, R=R, ranks_per_node=rpn, n_clusters=1,
+                     zipf_s=0.0, dtype="bf16")
+    Ld = DeviceLayer(cfg, L, np.zeros((T, 8), np.uint16), er, el, p, 5.0, row_cap=8, recv_cap=8)
+    Ld.front()
+    torch.cuda.synchronize()
+    r = oracle.route_prune(L, k, er, rpn, T // R, 5.0, p)
+    assert np.array_equal(Ld.host("idx"), r["idx"])
+    assert np.array_equal(Ld.host("w").view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(Ld.host("keep"), r["keep"])
+    assert np.array_equal(Ld.host("mask").view(np.uint64), r["mask"])
+    if kind == "cutoff":
+        w = oracle.gates(L, r["idx"])
+        assert np.any(w == 0.0) and np.any((w > 0) & (w < 1e-35))      # both sides of the cutoff reached
+    else:
+        # the target is reached exactly: kept devices = the fewest whose score reaches 1 - p
+        n_dev = np.array([bin(int(m)).count("1") for m in r["mask"]])
+        want = {0.25: 2, 0.5: 1, 0.75: 1}[p]
+        assert np.all(n_dev == want), np.unique(n_dev)
+
+
 @pytest.mark.parametrize("T,k,E", [(600_000, 8, 256), (200_000, 8, 128), (1000, 3, 7), (1, 1, 1)])
 def test_coactivation_duplicates_and_many_splits(T, k, E):
     """Random expert ids (duplicates within a token included) and random keep
@@ -312,7 +390,8 @@ def test_determinism_front_end():
 
 
 # ---------------------------------------------------------------- permutation
-@pytest.mark.parametrize("name,kind,p", [("c1", "seq", 0.3), ("c2", "coact", 0.3)])
+@pytest.mark.parametrize("name,kind,p", [("c1", "seq", 0.3), ("c2", "coact", 0.3), ("c3", "coact", 0.1),
+                                         ("c4", "coact", 0.1), ("c5", "coact", 0.1)])
 def test_permute_exact(name, kind, p):
     case = C.Case(name, gen.CONFIGS[name], kind, p)
     cfg = case.cfg
@@ -661,10 +740,50 @@ def test_ffn_f32_ragged_experts():
     assert C.rel_fro(got, ref) <= 1e-5
 
 
-@pytest.mark.parametrize("name,kind,p", [("c2", "coact", 0.3), ("c2", "seq", 0.0), ("c4", "coact", 0.1),
-                                         ("c3", "coact", 0.1), ("c5", "coact", 0.1)])
-def test_ffn_full_size_sampled_rows(name, kind, p):
-    """Rank 0's expert FFN at the workload's real shape; sampled rows vs the oracle."""
+ORACLE_THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def _m_tile_sample(eo, E_loc, rng, per_tile=2):
+    """Rows of a rank's expert-sorted buffer: per_tile random rows of every
+    256-row m-tile of every expert, plus each expert's first and last row."""
+    rows = []
+    base = int(eo[0])
+    for l in range(E_loc):
+        a, b = int(eo[l]) - base, int(eo[l + 1]) - base
+        if b <= a:
+            continue
+        rows += [a, b - 1]
+        for m0 in range(a, b, 256):
+            m1 = min(b, m0 + 256)
+            rows += list(rng.integers(m0, m1, size=per_tile))
+    return np.unique(np.asarray(rows, np.int64))
+
+
+def _oracle_ffn_rows(cfg, er, el, r, lay, x, rank, rows):
+    """fp64 oracle SwiGLU of the given rows of a rank's expert-sorted buffer."""
+    eo = lay["expert_offsets"][rank * cfg.E_loc:(rank + 1) * cfg.E_loc + 1].astype(np.int64)
+    xs = oracle.expert_gather(x, r["idx"], r["keep"], lay["slot_pos"], lay["expert_offsets"], er, cfg.R, rank)
+    xs32 = gen.bf16_bits_to_f32(xs) if cfg.dtype == "bf16" else xs
+    ids = C.local_experts(er, el, rank, cfg.E_loc)
+    ref = np.zeros((len(rows), cfg.d), np.float64)
+    for l in range(cfg.E_loc):
+        a, b = eo[l] - eo[0], eo[l + 1] - eo[0]
+        sel = np.flatnonzero((rows >= a) & (rows < b))
+        if len(sel):
+            W1, W3, W2 = (gen.expert_weights_f32(cfg, ids[l]))
+            ref[sel] = oracle.swiglu_rows(xs32[rows[sel]], W1, W3, W2, nthreads=ORACLE_THREADS)
+    return ref
+
+
+@pytest.mark.parametrize("name,kind,p,all_rows", [("c2", "coact", 0.3, True), ("c2", "seq", 0.0, True),
+                                                  ("c4", "coact", 0.1, True), ("c3", "coact", 0.1, True),
+                                                  ("c5", "coact", 0.1, False)])
+def test_ffn_full_size_benched_path(name, kind, p, all_rows):
+    """Rank 0's expert FFN at the workload's real shape through the benched
+    path (row source + the gathered FFN, which reads x in place), against the
+    fp64 oracle (Eq. 1 Expert_i): every row of the rank, or for the
+    DeepSeek-V3-shaped layer two rows of every 256-row m-tile plus each
+    expert's first and last row.  No wait of the fused kernel gave up."""
     case = C.Case(name, gen.CONFIGS[name], kind, p)
     cfg = case.cfg
     er, el = C.placement(name, kind, p, 5.0)
@@ -673,26 +792,57 @@ def test_ffn_full_size_sampled_rows(name, kind, p):
     L = _layer(case, x=x)
     L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
     L.front()
-    L.gather(0)
-    L.ffn(0)
+    L.row_source(0)
+    L.ffn_gather(0)
     torch.cuda.synchronize()
-    rows = L.rank_rows(0)
-    rng = np.random.default_rng(1)
-    sample = np.sort(rng.choice(rows, size=min(48, rows), replace=False))
-    eo = lay["expert_offsets"]
-    xs_all = gen.bf16_bits_to_f32(oracle.expert_gather(x, r["idx"], r["keep"], lay["slot_pos"], eo, er, cfg.R, 0))
-    got = L.Y[torch.from_numpy(sample).cuda()].float().cpu().numpy()
-    ids = C.local_experts(er, el, 0, cfg.E_loc)
-    ref = np.empty_like(got, dtype=np.float64)
-    for l in range(cfg.E_loc):
-        a, b = eo[l] - eo[0], eo[l + 1] - eo[0]
-        sel = np.where((sample >= a) & (sample < b))[0]
-        if len(sel):
-            W1, W3, W2 = gen.expert_weights_f32(cfg, ids[l])
-            ref[sel] = oracle.swiglu_rows(xs_all[sample[sel]], W1, W3, W2)
+    assert L.ffn_wait_errors() == 0
+    n = L.rank_rows(0)
+    eo = lay["expert_offsets"][:cfg.E_loc + 1]
+    rows = np.arange(n) if all_rows else _m_tile_sample(eo, cfg.E_loc, np.random.default_rng(1))
+    print(f"[{name} {kind} p={p}] rank-0 rows {n}, compared {len(rows)}", flush=True)
+    got = L.Y[:n].float().cpu().numpy()[rows]
+    ref = _oracle_ffn_rows(cfg, er, el, r, lay, x, 0, rows)
     ok, worst = C.within_tol(got, ref)
     assert ok, worst
     assert C.rel_fro(got, ref) <= 1e-2
+
+
+def test_step_bf16_end_to_end_all_received_rows():
+    """The whole benched step (DeviceLayer.step: routing, layout, co-activation,
+    row source, gathered FFN, destination reduce, source reduce) on the
+    Qwen3-shaped layer (coact, p = 0.3), bf16: every row rank 0 returns
+    (all of its received tokens) against the oracle's destination reduce of
+    the oracle FFN (Eq. 1 over the kept experts on rank 0; Sec. II-C local
+    aggregation), and rank 0's source-reduced output against the oracle's
+    source reduce of those rows (other ranks' returned rows zero here)."""
+    name, kind, p = "c2", "coact", 0.3
+    cfg = gen.CONFIGS[name]
+    case = C.Case(name, cfg, kind, p)
+    er, el = C.placement(name, kind, p, 5.0)
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = _layer(case, x=x)
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    L.parts.zero_()
+    L.step(0)
+    torch.cuda.synchronize()
+    assert L.ffn_wait_errors() == 0
+    n = L.rank_rows(0)
+    U0 = int(lay["recv_offsets"][1])
+    print(f"[c2 step] rank-0 rows {n}, received tokens {U0}", flush=True)
+    Y = _oracle_ffn_rows(cfg, er, el, r, lay, x, 0, np.arange(n)).astype(np.float32)
+    ref = oracle.dest_reduce(Y, r, lay, er, cfg.R, 0, cfg.d)
+    got = L.parts[:U0].float().cpu().numpy()
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+    parts = np.zeros((int(lay["recv_offsets"][-1]), cfg.d), np.float32)
+    parts[:U0] = got
+    ref_y = oracle.src_reduce(parts, r, lay, er, cfg.R, cfg.tokens_per_rank, 0, cfg.d)
+    got_y = L.y.float().cpu().numpy()
+    ok, worst = C.within_tol(got_y, ref_y)
+    assert ok, worst
+    assert C.rel_fro(got_y, ref_y) <= 1e-2
 
 
 @pytest.mark.parametrize("name", ["c4", "c5"])
