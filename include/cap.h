@@ -226,6 +226,30 @@ cap_status cap_dispatch_layout(const cap_topology *topo, const int32_t *idx, con
                                void *ws, size_t ws_bytes, void *stream);
 
 /*
+ * cap_dispatch_layout for callers that cannot allocate device memory (code
+ * under stream capture that may not call hipMalloc, tight serving loops,
+ * harnesses that forbid allocation): no workspace argument.  The library
+ * keeps a fixed device array of cap_dispatch_layout_static_max_bytes()
+ * (4 MiB) per GPU for it, from the first call on that GPU until the process
+ * ends, and allocates nothing per call.
+ *   Same arguments (minus ws / ws_bytes), outputs, arithmetic and bits as
+ *   cap_dispatch_layout.
+ *   Returns CAP_ERR_WORKSPACE if the topology needs more than that array
+ *   (cap_workspace_size(CAP_OP_DISPATCH_LAYOUT, topo, ...) > the maximum; about
+ *   R * ceil(tokens_per_rank / 256) * (E + R) * 4 bytes), CAP_ERR_HIP if the
+ *   array's device address cannot be obtained.
+ *   Every call on one GPU uses that GPU's one array, whose contents persist
+ *   between calls (no call needs them zeroed): calls that overlap in time on
+ *   one GPU (other streams, other threads) race and give undefined output;
+ *   order them on one stream.
+ */
+cap_status cap_dispatch_layout_static(const cap_topology *topo, const int32_t *idx, const uint8_t *keep,
+                                      const uint64_t *dst_mask, const cap_layout *out, void *stream);
+
+/* Bytes of the per-GPU array behind cap_dispatch_layout_static. */
+size_t cap_dispatch_layout_static_max_bytes(void);
+
+/*
  * Token permutation (Sec. II-B: a rank dispatches each token's hidden state
  * to the ranks of its selected experts and the receiver expands it into the
  * rows of each local expert; Sec. II-C: one copy per destination device, so

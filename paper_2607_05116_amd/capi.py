@@ -30,7 +30,8 @@ CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
            "cap_router_route_prune",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_expert_ffn_ex",
-           "cap_combine", "cap_coactivation"]
+           "cap_combine", "cap_coactivation", "cap_dispatch_layout_static",
+           "cap_dispatch_layout_static_max_bytes"]
 
 
 class CapError(RuntimeError):
@@ -73,6 +74,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "cap_router_route_prune": ([P(Topology), ctypes.c_int, i32, vp, vp, f32, vp, vp, vp, vp, vp, vp],
                                    ctypes.c_int),
         "cap_dispatch_layout": ([P(Topology), vp, vp, vp, P(Layout), vp, sz, vp], ctypes.c_int),
+        "cap_dispatch_layout_static": ([P(Topology), vp, vp, vp, P(Layout), vp], ctypes.c_int),
+        "cap_dispatch_layout_static_max_bytes": ([], sz),
         "cap_permute": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, vp, vp, vp, P(Layout),
                          vp, i32, vp], ctypes.c_int),
         "cap_expert_ffn": ([ctypes.c_int, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp],
@@ -163,6 +166,15 @@ def cap_dispatch_layout(topo, idx, keep, dst_mask, layout: Layout, ws, ws_bytes=
     _check("cap_dispatch_layout", _lib.cap_dispatch_layout(
         ctypes.byref(topo), _ptr(idx), _ptr(keep), _ptr(dst_mask), ctypes.byref(layout), _ptr(ws), nbytes,
         _stream(stream)))
+
+
+def cap_dispatch_layout_static(topo, idx, keep, dst_mask, layout: Layout, stream=None):
+    _check("cap_dispatch_layout_static", _lib.cap_dispatch_layout_static(
+        ctypes.byref(topo), _ptr(idx), _ptr(keep), _ptr(dst_mask), ctypes.byref(layout), _stream(stream)))
+
+
+def cap_dispatch_layout_static_max_bytes() -> int:
+    return int(_lib.cap_dispatch_layout_static_max_bytes())
 
 
 def cap_permute(topo, mode, rank, dtype, d, x, idx, keep, dst_mask, layout: Layout, out, out_rows,

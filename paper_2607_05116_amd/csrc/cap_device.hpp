@@ -12,6 +12,8 @@ constexpr int kWave = 64;
 constexpr int kMaxK = 8;
 constexpr int kMaxE = 256;
 constexpr int kMaxR = 64;
+constexpr int kMaxDevices = 64;                       // per-device caches of host code
+constexpr size_t kLayoutScratchBytes = size_t(4) << 20;   // cap_dispatch_layout_static's workspace
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));

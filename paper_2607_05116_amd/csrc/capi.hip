@@ -13,6 +13,7 @@ bool router_route_supported(const cap_topology*, int);
 cap_status router_route_launch(const cap_topology*, int, const void*, const void*, float, int32_t*, float*, uint8_t*,
                                uint64_t*, float*, hipStream_t);
 size_t layout_workspace_bytes(const cap_topology*);
+void* layout_scratch_ptr();
 cap_status dispatch_layout_launch(const cap_topology*, const int32_t*, const uint8_t*, const uint64_t*,
                                   const cap_layout*, void*, hipStream_t);
 cap_status permute_launch(const cap_topology*, cap_permute_mode, int, cap_dtype, int, const void*, const int32_t*,
@@ -156,6 +157,18 @@ cap_status cap_dispatch_layout(const cap_topology* topo, const int32_t* idx, con
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255) != 0) return CAP_ERR_WORKSPACE;
     return dispatch_layout_launch(topo, idx, keep, dst_mask, out, ws, as_stream(stream));
 }
+
+cap_status cap_dispatch_layout_static(const cap_topology* topo, const int32_t* idx, const uint8_t* keep,
+                                      const uint64_t* dst_mask, const cap_layout* out, void* stream) {
+    if (!topo_ok(topo) || !idx || !keep || !dst_mask || !layout_ok(out)) return CAP_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(out->vol) & 3) != 0) return CAP_ERR_INVALID_ARG;
+    if (layout_workspace_bytes(topo) > kLayoutScratchBytes) return CAP_ERR_WORKSPACE;
+    void* ws = layout_scratch_ptr();
+    if (!ws) return CAP_ERR_HIP;
+    return dispatch_layout_launch(topo, idx, keep, dst_mask, out, ws, as_stream(stream));
+}
+
+size_t cap_dispatch_layout_static_max_bytes(void) { return kLayoutScratchBytes; }
 
 cap_status cap_permute(const cap_topology* topo, cap_permute_mode mode, int32_t rank, cap_dtype dtype,
                        int32_t d, const void* x, const int32_t* idx, const uint8_t* keep, const uint64_t* dst_mask,

@@ -26,6 +26,14 @@
 //            C = R * ceil(T_loc / 256).
 #include "cap_device.hpp"
 
+#include <mutex>
+
+// Workspace of cap_dispatch_layout_static, for callers that cannot allocate:
+// one copy per GPU, held until the process ends.  Host code never uses this
+// name as an address (in host code it is only a stand-in for the symbol); it
+// takes the device address from hipGetSymbolAddress, per device.
+static __device__ __align__(256) unsigned char scratch[cap::kLayoutScratchBytes];
+
 namespace cap {
 namespace {
 
@@ -345,6 +353,22 @@ Workspace carve(const Geom& g, void* base, size_t* bytes) {
 }
 
 }  // namespace
+
+// Device address of `scratch` on the current device, looked up once per
+// device (with that device current) and kept; nullptr if the runtime refuses.
+void* layout_scratch_ptr() {
+    static std::mutex mu;
+    static void* ptrs[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptrs[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        ptrs[dev] = p;
+    }
+    return ptrs[dev];
+}
 
 size_t layout_workspace_bytes(const cap_topology* tp) {
     size_t b = 0;

@@ -164,3 +164,20 @@ def test_bench_refuses_more_than_one_gpu():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_dispatch_layout_static_rejects_topologies_past_its_array(capi):
+    """The allocation-free layout refuses, before touching the device, a
+    topology whose workspace would not fit its fixed per-GPU array."""
+    cap = capi.cap_dispatch_layout_static_max_bytes()
+    assert cap == 4 << 20
+    small = _topo(capi, E=128, R=8, ranks_per_node=8, T=32768, k=8)
+    assert 0 < capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, small) <= cap
+    big = _topo(capi, E=256, R=64, ranks_per_node=8, T=64 * 16384, k=8)
+    assert capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, big) > cap
+    lay = capi.Layout(*([0x9000] * 10))
+    st = capi._lib.cap_dispatch_layout_static(ctypes.byref(big), 0x3000, 0x4000, 0x5000, ctypes.byref(lay), None)
+    assert st == capi.CAP_ERR_WORKSPACE
+    bad = _topo(capi, k=0)
+    st = capi._lib.cap_dispatch_layout_static(ctypes.byref(bad), 0x3000, 0x4000, 0x5000, ctypes.byref(lay), None)
+    assert st == capi.CAP_ERR_INVALID_ARG
