@@ -114,25 +114,45 @@ def product_placement(cfg, p, c):
     return er, el, C
 
 
-def placement_spectrum(L, cfg, C, er, el, c):
-    """CAP offline step 3 (Sec. V): the Adjustment Approach's placement
-    spectrum from the co-activation placement, 7 points evaluated on this
-    workload's pruned routing (devices per token, load imbalance of kept rows,
-    send volume) next to the sequential placement.  Untimed; restores the
-    placement afterwards."""
+def placement_spectrum(cfg, p, c):
+    """CAP offline step 3 (Sec. V) on this workload: the Adjustment Approach's
+    swap sequence computed on the GPU (cap_adjustment_spectrum) from the
+    co-activation placement of the pruned trace, timed; then 7 points of the
+    spectrum and the sequential placement, each re-routed and re-laid-out on
+    the GPU over the evaluated batch (devices per token, load imbalance of kept
+    rows, send volume) with C(pi) on the trace's p_ij.  Untimed otherwise."""
+    import dataclasses
     import numpy as np
     import torch
     from paper_2607_05116_amd import placement
+    from paper_2607_05116_amd.layer import DeviceLayer
     from workloads import generator as gen
-    spec = placement.adjustment_spectrum(C, er, el, cfg.R, cfg.ranks_per_node, c)
+    er0, el0 = gen.sequential_placement(cfg)
+    tcfg = dataclasses.replace(cfg, T=cfg.trace_tokens, d=8)
+    Lt = DeviceLayer(tcfg, gen.trace_logits(cfg), np.zeros((tcfg.T, 8), np.uint16), er0, el0, p, c,
+                     row_cap=8, recv_cap=8)
+    Lt.route()
+    Lt.coactivation()
+    torch.cuda.synchronize()
+    C = Lt.host("coact").view(np.uint32)
+    er, el = placement.coactivation_placement(C, cfg.R, cfg.ranks_per_node, gen.random_order(cfg.E, 0, 0),
+                                              gen.random_order(cfg.R, 0, 1))
+    placement.adjustment_spectrum_gpu(Lt.coact, er, el, cfg.R, cfg.ranks_per_node, c)      # warm
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    spec, deltas = placement.adjustment_spectrum_gpu(Lt.coact, er, el, cfg.R, cfg.ranks_per_node, c)
+    build_s = time.perf_counter() - t0
     P = placement.coactivation_probability(C)
+    ecfg = dataclasses.replace(cfg, d=8)
+    Le = DeviceLayer(ecfg, gen.logits(cfg), np.zeros((cfg.T, 8), np.uint16), er, el, p, c, row_cap=8, recv_cap=8)
+
     def evaluate(ranks, local):
-        L.set_placement(ranks, local)
-        L.route()
-        L.layout()
+        Le.set_placement(ranks, local)
+        Le.route()
+        Le.layout()
         torch.cuda.synchronize()
-        tot = L.host("totals").astype(np.int64)
-        rows = np.diff(L.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
+        tot = Le.host("totals").astype(np.int64)
+        rows = np.diff(Le.host("expert_offsets")[:: cfg.E_loc]).astype(np.float64)
         return {"comm_objective": float(placement.comm_objective(P, np.asarray(ranks), cfg.ranks_per_node, c)),
                 "device_per_token": int(tot[0]) / cfg.T,
                 "load_imbalance": float(rows.max() / rows.mean()),
@@ -142,12 +162,9 @@ def placement_spectrum(L, cfg, C, er, el, c):
         pt = evaluate(spec[i][0], spec[i][1])
         pt["swaps"] = i
         points.append(pt)
-    seq = evaluate(*gen.sequential_placement(cfg))
-    L.set_placement(er, el)
-    L.route()
-    L.layout()
-    torch.cuda.synchronize()
-    return {"total_swaps": len(spec) - 1, "points": points, "sequential": seq}
+    seq = evaluate(er0, el0)
+    return {"zipf_s": cfg.zipf_s, "total_swaps": len(spec) - 1, "gpu_build_s": build_s,
+            "objective_increase_total": float(np.sum(deltas)), "points": points, "sequential": seq}
 
 
 def fused_front_end(L, cfg, stream, reps=20):
@@ -210,6 +227,8 @@ def cpu_baseline(cfg, p, c, logits, x, stride):
     import oracle
     from oracle import placement as oplace
     from workloads import generator as gen
+    # the FFN's OpenMP threads: the host's CPUs, capped at the 16 a GPU job
+    # gets on the box (cores = the threads it actually used)
     threads = min(16, os.cpu_count() or 1)
     er0, _ = gen.sequential_placement(cfg)
     tr = oracle.route_prune(gen.trace_logits(cfg), cfg.k, er0, cfg.ranks_per_node,
@@ -259,6 +278,8 @@ def cpu_baseline(cfg, p, c, logits, x, stride):
         "value": cfg.tokens_per_rank / total,
         "unit": "tokens/s",
         "cores": threads,
+        "threads_by_stage": {"routing_layout_coactivation": 1, "gather": 1, "ffn": threads, "combine": 1},
+        "host_logical_cpus": os.cpu_count(),
         "kind": "oracle",
         "sample": (f"full routing/layout/co-activation of all {cfg.T} tokens ({t_front:.2f} s, 1 thread), "
                    f"rank-0 gather ({t_gather:.2f} s), fp64 SwiGLU on every {stride}th of {rows0} rank-0 rows "
@@ -539,7 +560,7 @@ def main():
         },
     }
     if not args.quick:
-        result["aux"].update(detail_measurements(args, L, cfg, rank, stream, coact_counts, er, el, totals))
+        result["aux"].update(detail_measurements(args, L, cfg, rank, stream, totals))
     if not args.no_cpu:
         log("timing the CPU oracle on a bounded sample ...")
         result["cpu_baseline"] = cpu_baseline(cfg, args.p, args.c, logits, x, args.cpu_stride)
@@ -552,7 +573,7 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def detail_measurements(args, L, cfg, rank, stream, coact_counts, er, el, totals):
+def detail_measurements(args, L, cfg, rank, stream, totals):
     """Untimed detail of the headline workload: per-stage device times and
     HBM rates, CAP against expert-level pruning, the pruning sweep, the
     placement spectrum and the fused router front end."""
@@ -643,11 +664,15 @@ def detail_measurements(args, L, cfg, rank, stream, coact_counts, er, el, totals
     L.route()
     L.layout()
     torch.cuda.synchronize()
-    spectrum = None
-    if args.placement == "coact":
+    # the Adjustment Approach's spectrum on the stated workload and on the same
+    # layer with flatter expert popularity (Zipf 0.3)
+    import dataclasses
+    spectrum = {}
+    for label, scfg in (("stated", cfg), ("zipf_0.3", dataclasses.replace(cfg, zipf_s=0.3))):
         t_spec = time.perf_counter()
-        spectrum = placement_spectrum(L, cfg, coact_counts, er, el, args.c)
-        log(f"placement spectrum: {spectrum['total_swaps']} swaps, {time.perf_counter() - t_spec:.1f} s")
+        spectrum[label] = placement_spectrum(scfg, args.p, args.c)
+        log(f"placement spectrum ({label}): {spectrum[label]['total_swaps']} swaps in "
+            f"{spectrum[label]['gpu_build_s'] * 1e3:.2f} ms on the GPU; evaluated in {time.perf_counter() - t_spec:.1f} s")
 
     front_end = fused_front_end(L, cfg, stream)
     return {"stage_ms": stage_ms, "stage_hbm_GBs": hbm, "pruning_cap_vs_naive": pruning,

@@ -72,7 +72,8 @@ typedef enum {
     CAP_OP_PERMUTE = 2,
     CAP_OP_EXPERT_FFN = 3,
     CAP_OP_COMBINE = 4,
-    CAP_OP_COACTIVATION = 5
+    CAP_OP_COACTIVATION = 5,
+    CAP_OP_ADJUSTMENT = 6
 } cap_op;
 
 /*
@@ -153,6 +154,7 @@ int32_t cap_version(void);
  *   CAP_OP_EXPERT_FFN: the SwiGLU intermediate H, max_rows x inter values of
  *                      `dtype` (topo and d unused, may be NULL / 0).
  *   CAP_OP_COACTIVATION: per-split partial counts (uses topo->T and topo->E).
+ *   CAP_OP_ADJUSTMENT: the E x E fp64 co-activation ratios (uses topo->E).
  *   Other ops need none.
  * Returns 0 for invalid arguments as well.
  */
@@ -397,6 +399,38 @@ cap_status cap_combine(const cap_topology *topo, cap_combine_mode mode, int32_t 
 cap_status cap_coactivation(int32_t T, int32_t k, int32_t E, const int32_t *idx,
                             const uint8_t *keep, uint32_t *coact, int32_t accumulate,
                             void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Adjustment Approach (Sec. V: trade communication for load balance by
+ * swapping experts between the most and the least loaded devices, keeping as
+ * much co-activation locality as possible; Eq. 2-3 objective C, Eq. 4 loads),
+ * run on the GPU from a communication-oriented placement.
+ *   coact[E][E]        (device) co-activation counts of a pruned routing trace
+ *                      (cap_coactivation): N_e = coact[e][e] is expert e's load
+ *                      in rows; p_ij = C_ij / (N_i + N_j - C_ij), 0 when the
+ *                      denominator is 0.
+ *   expert_rank[E], expert_local[E] (device, in/out) the starting placement
+ *                      (a bijection onto [0,R) x [0,E/R)); on return the
+ *                      placement after the last swap.
+ *   Each step: hi = most loaded device, lo = least loaded (ties: lower id; the
+ *   spectrum ends when their loads are equal); candidates e on hi and f on lo
+ *   with N_e > N_f and L_lo + N_e - N_f < L_hi; the chosen one has the smallest
+ *   increase of C (ties: lower e, then lower f), summed in fp64 over every
+ *   other expert j, ascending, as p_ej (d(lo, pi_j) - d(hi, pi_j)) then
+ *   p_fj (d(hi, pi_j) - d(lo, pi_j)), d = 0 / 1 / inter_node_cost (Eq. 3);
+ *   e and f exchange devices and local slots.  Stops when no candidate
+ *   remains or after max_swaps swaps.
+ *   swaps[max_swaps][2] (device) the (e, f) of each swap, in order;
+ *   deltas[max_swaps]  (device, nullable) each swap's increase of C;
+ *   n_swaps            (device int32) swaps made.
+ * Workspace: cap_workspace_size(CAP_OP_ADJUSTMENT, topo with this E, ...),
+ * 8-byte aligned.  Needs 1 <= E <= 256, 1 <= R <= 64, E % R == 0,
+ * R % ranks_per_node == 0, inter_node_cost >= 1, max_swaps >= 0.
+ */
+cap_status cap_adjustment_spectrum(const uint32_t *coact, int32_t E, int32_t R, int32_t ranks_per_node,
+                                   float inter_node_cost, int32_t *expert_rank, int32_t *expert_local,
+                                   int32_t max_swaps, int32_t *swaps, double *deltas, int32_t *n_swaps,
+                                   void *ws, size_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

@@ -137,8 +137,12 @@ def load_imbalance(loads):
 #   swap lowers the larger of the two loads (N_e > N_f and
 #   L_lo + N_e - N_f < L_hi);
 # * the chosen pair has the smallest increase of the communication objective
-#   (Eq. 2-3, recomputed from its definition; ties: lower e, then lower f);
-#   e and f exchange devices and local slots;
+#   (Eq. 2-3; ties: lower e, then lower f); e and f exchange devices and
+#   local slots.  The increase is summed over the pairs whose distance the
+#   swap changes -- (e, j) and (f, j) for every other expert j, in ascending
+#   j, the e term before the f term -- which equals the difference of the two
+#   objectives without the cancellation of subtracting two full sums (the
+#   pair (e, f) keeps its distance);
 # * the spectrum ends when no candidate remains (or after max_swaps).
 
 def expert_loads(C):
@@ -152,6 +156,31 @@ def device_loads(N, expert_rank, R):
     return L
 
 
+def distance(a, b, ranks_per_node, c):
+    """Eq. 3: d = 0 on one device, 1 within a node, c across nodes."""
+    if a == b:
+        return 0.0
+    if a // ranks_per_node == b // ranks_per_node:
+        return 1.0
+    return float(c)
+
+
+def swap_delta(P, expert_rank, e, f, ranks_per_node, c):
+    """Increase of the Eq. 2-3 objective when e (on device hi) and f (on lo)
+    exchange devices: sum over every other expert j, ascending, of
+    p_ej (d(lo, pi_j) - d(hi, pi_j)) and then p_fj (d(hi, pi_j) - d(lo, pi_j))."""
+    hi, lo = expert_rank[e], expert_rank[f]
+    delta = 0.0
+    for j in range(len(P)):
+        if j == e or j == f:
+            continue
+        g = expert_rank[j]
+        a = distance(lo, g, ranks_per_node, c) - distance(hi, g, ranks_per_node, c)
+        delta += P[e][j] * a
+        delta += P[f][j] * -a
+    return delta
+
+
 def adjust_step(P, N, expert_rank, expert_local, R, ranks_per_node, c):
     """One swap -> (expert_rank, expert_local, (e, f), delta_C), or None."""
     L = device_loads(N, expert_rank, R)
@@ -159,7 +188,6 @@ def adjust_step(P, N, expert_rank, expert_local, R, ranks_per_node, c):
     lo = min(range(R), key=lambda g: (L[g], g))
     if L[hi] == L[lo]:
         return None
-    base = comm_objective(P, expert_rank, ranks_per_node, c)
     best = None
     for e in range(len(N)):
         if expert_rank[e] != hi:
@@ -169,9 +197,7 @@ def adjust_step(P, N, expert_rank, expert_local, R, ranks_per_node, c):
                 continue
             if not (N[e] > N[f] and L[lo] + N[e] - N[f] < L[hi]):
                 continue
-            trial = list(expert_rank)
-            trial[e], trial[f] = lo, hi
-            delta = comm_objective(P, trial, ranks_per_node, c) - base
+            delta = swap_delta(P, expert_rank, e, f, ranks_per_node, c)
             if best is None or delta < best[2]:
                 best = (e, f, delta)
     if best is None:

@@ -25,13 +25,13 @@ CAP_DTYPE_F32, CAP_DTYPE_BF16 = 0, 1
 CAP_PERMUTE_EXPERT_GATHER, CAP_PERMUTE_SEND_PACK, CAP_PERMUTE_ROW_SOURCE = 0, 1, 2
 CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 (CAP_OP_ROUTE_PRUNE, CAP_OP_DISPATCH_LAYOUT, CAP_OP_PERMUTE, CAP_OP_EXPERT_FFN,
- CAP_OP_COMBINE, CAP_OP_COACTIVATION) = range(6)
+ CAP_OP_COMBINE, CAP_OP_COACTIVATION, CAP_OP_ADJUSTMENT) = range(7)
 
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
            "cap_router_route_prune",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_expert_ffn_ex",
            "cap_combine", "cap_coactivation", "cap_dispatch_layout_static",
-           "cap_dispatch_layout_static_max_bytes"]
+           "cap_dispatch_layout_static_max_bytes", "cap_adjustment_spectrum"]
 
 
 class CapError(RuntimeError):
@@ -87,6 +87,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "cap_combine": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, i32, vp, vp, vp, vp,
                          P(Layout), vp, vp, i32, vp], ctypes.c_int),
         "cap_coactivation": ([i32, i32, i32, vp, vp, vp, i32, vp, sz, vp], ctypes.c_int),
+        "cap_adjustment_spectrum": ([vp, i32, i32, i32, f32, vp, vp, i32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -225,3 +226,12 @@ def cap_coactivation(T, k, E, idx, keep, coact, accumulate, ws, ws_bytes=None, s
     nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
     _check("cap_coactivation", _lib.cap_coactivation(
         T, k, E, _ptr(idx), _ptr(keep), _ptr(coact), int(accumulate), _ptr(ws), nbytes, _stream(stream)))
+
+
+def cap_adjustment_spectrum(coact, E, R, ranks_per_node, inter_node_cost, expert_rank, expert_local, max_swaps,
+                            swaps, deltas, n_swaps, ws, ws_bytes=None, stream=None):
+    nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
+    _check("cap_adjustment_spectrum", _lib.cap_adjustment_spectrum(
+        _ptr(coact), int(E), int(R), int(ranks_per_node), float(inter_node_cost), _ptr(expert_rank),
+        _ptr(expert_local), int(max_swaps), _ptr(swaps), _ptr(deltas), _ptr(n_swaps), _ptr(ws), nbytes,
+        _stream(stream)))

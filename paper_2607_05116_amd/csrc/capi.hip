@@ -27,6 +27,9 @@ cap_status expert_ffn_launch(cap_dtype, int, int, int, int, const void*, int, co
                              const void*, const void*, const void*, void*, void*, const cap_ffn_options*,
                              hipStream_t);
 size_t coact_workspace_bytes(int, int);
+size_t adjustment_workspace_bytes(int);
+cap_status adjustment_launch(const uint32_t*, int, int, int, float, int32_t*, int32_t*, int, int32_t*, double*,
+                             int32_t*, void*, hipStream_t);
 cap_status coactivation_launch(int, int, int, const int32_t*, const uint8_t*, uint32_t*, int, void*,
                                hipStream_t);
 
@@ -118,6 +121,9 @@ size_t cap_workspace_size(cap_op op, const cap_topology* topo, int32_t d, int32_
         case CAP_OP_COACTIVATION:
             if (!topo || topo->T < 1 || topo->E < 1 || topo->E > kMaxE) return 0;
             return coact_workspace_bytes(topo->T, topo->E);
+        case CAP_OP_ADJUSTMENT:
+            if (!topo || topo->E < 1 || topo->E > kMaxE) return 0;
+            return adjustment_workspace_bytes(topo->E);
         default:
             return 0;
     }
@@ -257,6 +263,21 @@ cap_status cap_coactivation(int32_t T, int32_t k, int32_t E, const int32_t* idx,
     if (!ws || ws_bytes < coact_workspace_bytes(T, E) || (reinterpret_cast<uintptr_t>(ws) & 15) != 0)
         return CAP_ERR_WORKSPACE;
     return coactivation_launch(T, k, E, idx, keep, coact, accumulate, ws, as_stream(stream));
+}
+
+cap_status cap_adjustment_spectrum(const uint32_t* coact, int32_t E, int32_t R, int32_t ranks_per_node,
+                                   float inter_node_cost, int32_t* expert_rank, int32_t* expert_local,
+                                   int32_t max_swaps, int32_t* swaps, double* deltas, int32_t* n_swaps, void* ws,
+                                   size_t ws_bytes, void* stream) {
+    if (!coact || !expert_rank || !expert_local || !swaps || !n_swaps) return CAP_ERR_INVALID_ARG;
+    if (E < 1 || E > kMaxE || R < 1 || R > kMaxR || E % R != 0) return CAP_ERR_INVALID_ARG;
+    if (ranks_per_node < 1 || R % ranks_per_node != 0 || max_swaps < 0) return CAP_ERR_INVALID_ARG;
+    if (!(inter_node_cost >= 1.0f) || !(inter_node_cost < INFINITY)) return CAP_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(deltas) & 7) != 0) return CAP_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < adjustment_workspace_bytes(E) || (reinterpret_cast<uintptr_t>(ws) & 7) != 0)
+        return CAP_ERR_WORKSPACE;
+    return adjustment_launch(coact, E, R, ranks_per_node, inter_node_cost, expert_rank, expert_local, max_swaps,
+                             swaps, deltas, n_swaps, ws, as_stream(stream));
 }
 
 }  // extern "C"

@@ -115,20 +115,39 @@ def load_imbalance(loads) -> float:
 #              loaded one (ties: lower id);
 #   candidates e on the former, f on the latter, whose swap lowers the larger
 #              of the two loads (N_e > N_f, L_lo + N_e - N_f < L_hi);
-#   choice     smallest increase of the Eq. 2-3 objective, each candidate's
-#              objective summed sequentially over i < j in row-major order
-#              (ties: lower e, then lower f); e and f exchange local slots;
+#   choice     smallest increase of the Eq. 2-3 objective (ties: lower e,
+#              then lower f); e and f exchange local slots.  The increase is
+#              summed over the pairs whose distance changes: for every other
+#              expert j, ascending, p_ej (d(lo, pi_j) - d(hi, pi_j)) and then
+#              p_fj (d(hi, pi_j) - d(lo, pi_j)), sequentially in fp64;
 #   end        no candidate remains (or max_swaps).
+# cap_adjustment_spectrum runs the same swaps on the GPU.
 
-def _sequential_objectives(P: np.ndarray, ranks: np.ndarray, ranks_per_node: int, c: float) -> np.ndarray:
-    """Eq. 2-3 objective of each placement row of `ranks`, summed sequentially
-    over i < j in row-major order (so the rounding is the same for every row)."""
+def _distance_matrix(R: int, ranks_per_node: int, c: float) -> np.ndarray:
+    g = np.arange(R)
+    same_node = (g[:, None] // ranks_per_node) == (g[None, :] // ranks_per_node)
+    D = np.where(same_node, 1.0, float(c))
+    np.fill_diagonal(D, 0.0)
+    return D
+
+
+def swap_deltas(P: np.ndarray, er: np.ndarray, E2: np.ndarray, F2: np.ndarray, hi: int, lo: int,
+                ranks_per_node: int, c: float, R: int) -> np.ndarray:
+    """Objective increase of each candidate swap (E2[k] on hi <-> F2[k] on lo),
+    the terms of every other expert j in ascending j, e term then f term,
+    summed sequentially (one running sum per candidate)."""
+    D = _distance_matrix(R, ranks_per_node, c)
+    a = D[lo, er] - D[hi, er]                                # per expert j
     n = P.shape[0]
-    iu, ju = np.triu_indices(n, 1)
-    pv = P[iu, ju]
-    a, b = ranks[:, iu], ranks[:, ju]
-    dist = np.where(a == b, 0.0, np.where(a // ranks_per_node == b // ranks_per_node, 1.0, float(c)))
-    return np.cumsum(pv[None, :] * dist, axis=1)[:, -1]
+    terms = np.empty((len(E2), 2 * n))
+    terms[:, 0::2] = P[E2] * a[None, :]
+    terms[:, 1::2] = P[F2] * -a[None, :]
+    j = np.arange(n)
+    skip = (j[None, :] == E2[:, None]) | (j[None, :] == F2[:, None])
+    terms[:, 0::2][skip] = 0.0
+    terms[:, 1::2][skip] = 0.0
+    # a skipped term adds +0.0: the running sum is unchanged by it (x + 0.0 == x)
+    return np.cumsum(terms, axis=1)[:, -1]
 
 
 def adjustment_spectrum(C, expert_rank, expert_local, R: int, ranks_per_node: int, c: float,
@@ -153,18 +172,46 @@ def adjustment_spectrum(C, expert_rank, expert_local, R: int, ranks_per_node: in
         if not ok.any():
             break
         E2, F2 = E2[ok], F2[ok]
-        trial = np.repeat(er[None, :], len(E2), axis=0)
-        rows = np.arange(len(E2))
-        trial[rows, E2] = lo
-        trial[rows, F2] = hi
-        base = _sequential_objectives(P, er[None, :], ranks_per_node, c)[0]
-        delta = _sequential_objectives(P, trial, ranks_per_node, c) - base
+        delta = swap_deltas(P, er, E2, F2, hi, lo, ranks_per_node, c, R)
         k = int(np.argmin(delta))                           # first minimum: lower e, then f
         e, f = int(E2[k]), int(F2[k])
         er[e], er[f] = lo, hi
         el[e], el[f] = el[f], el[e]
         out.append((er.copy(), el.copy(), (e, f)))
     return out
+
+
+def adjustment_spectrum_gpu(coact, expert_rank, expert_local, R: int, ranks_per_node: int, c: float,
+                            max_swaps: int = 4096, stream=None):
+    """The Adjustment Approach on the GPU (cap_adjustment_spectrum): coact is
+    the int32/uint32 [E][E] co-activation counts on the device.  Returns the
+    same list as adjustment_spectrum (the placements are rebuilt on the host
+    from the swap sequence the kernel chose) and the per-swap increases."""
+    import torch
+    from . import capi
+    E = int(coact.shape[0])
+    dev = coact.device
+    er_d = torch.as_tensor(np.asarray(expert_rank, np.int32)).to(dev)
+    el_d = torch.as_tensor(np.asarray(expert_local, np.int32)).to(dev)
+    swaps = torch.empty((max(max_swaps, 1), 2), dtype=torch.int32, device=dev)
+    deltas = torch.empty(max(max_swaps, 1), dtype=torch.float64, device=dev)
+    n_swaps = torch.zeros(1, dtype=torch.int32, device=dev)
+    topo = capi.Topology(E=E, R=R, ranks_per_node=ranks_per_node, T=R, tokens_per_rank=1, k=1)
+    ws = torch.empty(capi.cap_workspace_size(capi.CAP_OP_ADJUSTMENT, topo), dtype=torch.uint8, device=dev)
+    capi.cap_adjustment_spectrum(coact, E, R, ranks_per_node, c, er_d, el_d, max_swaps, swaps, deltas, n_swaps,
+                                 ws, stream=stream)
+    n = int(n_swaps.item())
+    pairs = swaps[:n].cpu().numpy()
+    er = np.asarray(expert_rank, np.int32).copy()
+    el = np.asarray(expert_local, np.int32).copy()
+    out = [(er.copy(), el.copy(), None)]
+    for e, f in pairs:
+        e, f = int(e), int(f)
+        er[e], er[f] = er[f], er[e]
+        el[e], el[f] = el[f], el[e]
+        out.append((er.copy(), el.copy(), (e, f)))
+    assert np.array_equal(er, er_d.cpu().numpy()) and np.array_equal(el, el_d.cpu().numpy())
+    return out, deltas[:n].cpu().numpy()
 
 
 def spectrum_points(n_placements: int, points: int = 7) -> list[int]:

@@ -181,3 +181,16 @@ def test_dispatch_layout_static_rejects_topologies_past_its_array(capi):
     bad = _topo(capi, k=0)
     st = capi._lib.cap_dispatch_layout_static(ctypes.byref(bad), 0x3000, 0x4000, 0x5000, ctypes.byref(lay), None)
     assert st == capi.CAP_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("over", [dict(E=0), dict(E=300), dict(R=3), dict(R=65, E=130), dict(rpn=3),
+                                  dict(c=0.5), dict(max_swaps=-1)])
+def test_adjustment_rejects_bad_arguments(capi, over):
+    kw = dict(E=16, R=4, rpn=2, c=5.0, max_swaps=4)
+    kw.update(over)
+    st = capi._lib.cap_adjustment_spectrum(0x1000, kw["E"], kw["R"], kw["rpn"], kw["c"], 0x2000, 0x3000,
+                                           kw["max_swaps"], 0x4000, None, 0x5000, 0x6000, 1 << 20, None)
+    assert st == capi.CAP_ERR_INVALID_ARG
+    st = capi._lib.cap_adjustment_spectrum(0x1000, 16, 4, 2, 5.0, 0x2000, 0x3000, 4, 0x4000, None, 0x5000,
+                                           0x6000, 16 * 16 * 8 - 1, None)
+    assert st == capi.CAP_ERR_WORKSPACE

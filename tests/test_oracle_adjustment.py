@@ -66,6 +66,8 @@ def test_each_swap_is_an_exact_minimum(seed, R, rpn, c):
         best = min(delta(p) for p in cands)
         # the choice is an exact minimum (floating point may only split exact ties)
         assert delta((e, f)) == best
+        # and the reported increase is the exact objective difference, rounded
+        assert abs(float(delta((e, f))) - step[3]) <= 1e-12
         er, el = step[0], step[1]
         steps += 1
         assert steps < 100

@@ -61,7 +61,9 @@ MUTANTS = [
      "co-activation: counted on unpruned routing"),
     ("placement.py", "delta < best[2]", "delta <= best[2]", "adjustment: ties to the later candidate"),
     ("placement.py", "N[e] > N[f] and", "N[e] >= N[f] and", "adjustment: equal loads swapped"),
-    ("placement.py", "trial[e], trial[f] = lo, hi", "trial[e], trial[f] = hi, lo", "adjustment: swap not applied"),
+    ("placement.py", "delta += P[f][j] * -a", "delta += P[f][j] * a", "adjustment: sign of the f terms"),
+    ("placement.py", "if j == e or j == f:", "if j == e:", "adjustment: pair (e, f) counted as moved"),
+    ("placement.py", "er[e], er[f] = lo, hi", "er[e], er[f] = hi, lo", "adjustment: swap not applied"),
     ("placement.py", "el[e], el[f] = expert_local[f], expert_local[e]",
      "el[e], el[f] = expert_local[e], expert_local[f]", "adjustment: local slots not exchanged"),
 ]
