@@ -582,8 +582,9 @@ def detail_measurements(args, L, cfg, rank, stream, totals):
     # per-stage device times (separate, untimed): each stage captured as a graph
     # of 20 back-to-back calls (every stage rewrites the same buffers from
     # unchanged inputs) and replayed, so launch gaps do not enter the times
-    stages = ["route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather", "ffn_rows"]
-    fns = [L.route, L.layout, L.coactivation, lambda: L.row_source(rank), lambda: L.ffn_gather(rank),
+    stages = ["front_fused", "route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather",
+              "ffn_rows"]
+    fns = [L.route_layout, L.route, L.layout, L.coactivation, lambda: L.row_source(rank), lambda: L.ffn_gather(rank),
            lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank),
            lambda: L.gather(rank), lambda: L.ffn(rank)]
 

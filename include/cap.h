@@ -73,7 +73,8 @@ typedef enum {
     CAP_OP_EXPERT_FFN = 3,
     CAP_OP_COMBINE = 4,
     CAP_OP_COACTIVATION = 5,
-    CAP_OP_ADJUSTMENT = 6
+    CAP_OP_ADJUSTMENT = 6,
+    CAP_OP_ROUTE_LAYOUT = 7
 } cap_op;
 
 /*
@@ -155,6 +156,8 @@ int32_t cap_version(void);
  *                      `dtype` (topo and d unused, may be NULL / 0).
  *   CAP_OP_COACTIVATION: per-split partial counts (uses topo->T and topo->E).
  *   CAP_OP_ADJUSTMENT: the E x E fp64 co-activation ratios (uses topo->E).
+ *   CAP_OP_ROUTE_LAYOUT: per-32-token column counts, column totals, volume
+ *                      sums and co-activation partials (uses topo only).
  *   Other ops need none.
  * Returns 0 for invalid arguments as well.
  */
@@ -226,6 +229,23 @@ cap_status cap_router_route_prune(const cap_topology *topo, cap_dtype dtype, int
 cap_status cap_dispatch_layout(const cap_topology *topo, const int32_t *idx, const uint8_t *keep,
                                const uint64_t *dst_mask, const cap_layout *out,
                                void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * The routing front end fused (Eq. 1 top-k and gates; Sec. VI, Eq. 6 pruning;
+ * Sec. II-C layout and Eq. 3 volumes; Sec. IV-B co-activation on the pruned
+ * routing): cap_route_prune, then cap_dispatch_layout, then (if coact is not
+ * NULL) cap_coactivation overwriting coact, with the same outputs bit for bit,
+ * in three launches instead of six.  The routing kernel also counts each
+ * 32-token part's kept experts and devices (per-wave integer LDS counts
+ * summed in a fixed order) and the per-token volume, so the layout needs one
+ * scan and one scatter; the
+ * co-activation tiles run beside the scan, its reduce beside the scatter.
+ * Arguments as in those calls; coact [E][E] (device, nullable).  Workspace:
+ * cap_workspace_size(CAP_OP_ROUTE_LAYOUT, topo, ...), 256-byte aligned.
+ */
+cap_status cap_route_layout(const cap_topology *topo, const float *logits, float p, int32_t *idx, float *w,
+                            uint8_t *keep, uint64_t *dst_mask, const cap_layout *out, uint32_t *coact, void *ws,
+                            size_t ws_bytes, void *stream);
 
 /*
  * cap_dispatch_layout for callers that cannot allocate device memory (code

@@ -25,13 +25,13 @@ CAP_DTYPE_F32, CAP_DTYPE_BF16 = 0, 1
 CAP_PERMUTE_EXPERT_GATHER, CAP_PERMUTE_SEND_PACK, CAP_PERMUTE_ROW_SOURCE = 0, 1, 2
 CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
 (CAP_OP_ROUTE_PRUNE, CAP_OP_DISPATCH_LAYOUT, CAP_OP_PERMUTE, CAP_OP_EXPERT_FFN,
- CAP_OP_COMBINE, CAP_OP_COACTIVATION, CAP_OP_ADJUSTMENT) = range(7)
+ CAP_OP_COMBINE, CAP_OP_COACTIVATION, CAP_OP_ADJUSTMENT, CAP_OP_ROUTE_LAYOUT) = range(8)
 
 EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_prune", "cap_route_prune_naive",
            "cap_router_route_prune",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_expert_ffn_ex",
            "cap_combine", "cap_coactivation", "cap_dispatch_layout_static",
-           "cap_dispatch_layout_static_max_bytes", "cap_adjustment_spectrum"]
+           "cap_dispatch_layout_static_max_bytes", "cap_adjustment_spectrum", "cap_route_layout"]
 
 
 class CapError(RuntimeError):
@@ -87,6 +87,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "cap_combine": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, i32, vp, vp, vp, vp,
                          P(Layout), vp, vp, i32, vp], ctypes.c_int),
         "cap_coactivation": ([i32, i32, i32, vp, vp, vp, i32, vp, sz, vp], ctypes.c_int),
+        "cap_route_layout": ([P(Topology), vp, f32, vp, vp, vp, vp, P(Layout), vp, vp, sz, vp], ctypes.c_int),
         "cap_adjustment_spectrum": ([vp, i32, i32, i32, f32, vp, vp, i32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -167,6 +168,14 @@ def cap_dispatch_layout(topo, idx, keep, dst_mask, layout: Layout, ws, ws_bytes=
     _check("cap_dispatch_layout", _lib.cap_dispatch_layout(
         ctypes.byref(topo), _ptr(idx), _ptr(keep), _ptr(dst_mask), ctypes.byref(layout), _ptr(ws), nbytes,
         _stream(stream)))
+
+
+def cap_route_layout(topo, logits, p, idx, w, keep, dst_mask, layout: Layout, coact, ws, ws_bytes=None,
+                     stream=None):
+    nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
+    _check("cap_route_layout", _lib.cap_route_layout(
+        ctypes.byref(topo), _ptr(logits), float(p), _ptr(idx), _ptr(w), _ptr(keep), _ptr(dst_mask),
+        ctypes.byref(layout), _ptr(coact), _ptr(ws), nbytes, _stream(stream)))
 
 
 def cap_dispatch_layout_static(topo, idx, keep, dst_mask, layout: Layout, stream=None):

@@ -28,6 +28,9 @@ cap_status expert_ffn_launch(cap_dtype, int, int, int, int, const void*, int, co
                              hipStream_t);
 size_t coact_workspace_bytes(int, int);
 size_t adjustment_workspace_bytes(int);
+size_t front_end_workspace_bytes(const cap_topology*);
+cap_status front_end_launch(const cap_topology*, const float*, float, int32_t*, float*, uint8_t*, uint64_t*,
+                            const cap_layout*, uint32_t*, void*, hipStream_t);
 cap_status adjustment_launch(const uint32_t*, int, int, int, float, int32_t*, int32_t*, int, int32_t*, double*,
                              int32_t*, void*, hipStream_t);
 cap_status coactivation_launch(int, int, int, const int32_t*, const uint8_t*, uint32_t*, int, void*,
@@ -121,6 +124,8 @@ size_t cap_workspace_size(cap_op op, const cap_topology* topo, int32_t d, int32_
         case CAP_OP_COACTIVATION:
             if (!topo || topo->T < 1 || topo->E < 1 || topo->E > kMaxE) return 0;
             return coact_workspace_bytes(topo->T, topo->E);
+        case CAP_OP_ROUTE_LAYOUT:
+            return topo_ok(topo) ? front_end_workspace_bytes(topo) : 0;
         case CAP_OP_ADJUSTMENT:
             if (!topo || topo->E < 1 || topo->E > kMaxE) return 0;
             return adjustment_workspace_bytes(topo->E);
@@ -162,6 +167,17 @@ cap_status cap_dispatch_layout(const cap_topology* topo, const int32_t* idx, con
     const size_t need = layout_workspace_bytes(topo);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) & 255) != 0) return CAP_ERR_WORKSPACE;
     return dispatch_layout_launch(topo, idx, keep, dst_mask, out, ws, as_stream(stream));
+}
+
+cap_status cap_route_layout(const cap_topology* topo, const float* logits, float p, int32_t* idx, float* w,
+                            uint8_t* keep, uint64_t* dst_mask, const cap_layout* out, uint32_t* coact, void* ws,
+                            size_t ws_bytes, void* stream) {
+    if (!topo_ok(topo) || !logits || !idx || !w || !keep || !dst_mask || !layout_ok(out)) return CAP_ERR_INVALID_ARG;
+    if (!(p >= 0.0f) || !(p < 1.0f)) return CAP_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(out->vol) & 3) != 0) return CAP_ERR_INVALID_ARG;
+    if (!ws || ws_bytes < front_end_workspace_bytes(topo) || (reinterpret_cast<uintptr_t>(ws) & 255) != 0)
+        return CAP_ERR_WORKSPACE;
+    return front_end_launch(topo, logits, p, idx, w, keep, dst_mask, out, coact, ws, as_stream(stream));
 }
 
 cap_status cap_dispatch_layout_static(const cap_topology* topo, const int32_t* idx, const uint8_t* keep,

@@ -1,0 +1,354 @@
+// Kernels of the device-centric all-to-all layout, shared by the layout call
+// and the fused front end (see dispatch_layout.hip for the method).
+#pragma once
+
+#include "cap_device.hpp"
+
+namespace cap {
+namespace {
+
+
+constexpr int kChunk = 256;        // tokens per chunk = threads per block
+constexpr int kWavesPerChunk = kChunk / kWave;
+constexpr int kMaxW = kMaxE + kMaxR;
+
+// C chunks of up to kChunk tokens within one source rank (cpr per rank); the
+// per-chunk counts may come in `sub` partial rows per chunk (Cs = C * sub rows
+// of the workspace), each counting a consecutive part of the chunk.
+struct Geom {
+    int T, E, k, R, rpn, tpr, E_loc, cpr, C, W, sub, Cs;
+};
+
+struct Workspace {
+    int32_t* part;     // [Cs][W]
+    int32_t* coltot;   // [W]
+    int64_t* volpart;  // [Cs][4]
+};
+
+inline size_t align256(size_t b) { return (b + 255) & ~static_cast<size_t>(255); }
+
+__device__ __forceinline__ void chunk_range(const Geom& g, int c, int& t0, int& t1, int& src) {
+    src = c / g.cpr;
+    t0 = src * g.tpr + (c % g.cpr) * kChunk;
+    t1 = min(t0 + kChunk, (src + 1) * g.tpr);
+}
+
+__device__ __forceinline__ int slot_position(const int32_t* er, const int32_t* el, int e, const Geom& g) {
+    if (static_cast<unsigned>(e) >= static_cast<unsigned>(g.E)) return -1;
+    const int r = er[e], l = el[e];
+    if (static_cast<unsigned>(r) >= static_cast<unsigned>(g.R) ||
+        static_cast<unsigned>(l) >= static_cast<unsigned>(g.E_loc))
+        return -1;
+    return r * g.E_loc + l;
+}
+
+__device__ __forceinline__ uint64_t device_bits(uint64_t m, int R) {
+    return R >= 64 ? m : (m & ((1ull << R) - 1));
+}
+
+// Slot positions (-1 when pruned or invalid) and device mask of token t.
+__device__ __forceinline__ void load_token(const Geom& g, int t, const int32_t* __restrict__ idx,
+                                           const uint8_t* __restrict__ keep, const uint64_t* __restrict__ mask,
+                                           const int* pos_lds, int (&P)[kMaxK], uint64_t& m) {
+    int e[kMaxK];
+    uint8_t kp[kMaxK];
+    const size_t q0 = static_cast<size_t>(t) * g.k;
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s) {
+        e[s] = -1;
+        kp[s] = 0;
+        if (s < g.k) {
+            e[s] = idx[q0 + s];
+            kp[s] = keep[q0 + s];
+        }
+    }
+    m = device_bits(mask[t], g.R);
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s)
+        P[s] = (kp[s] && static_cast<unsigned>(e[s]) < static_cast<unsigned>(g.E)) ? pos_lds[e[s]] : -1;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Exclusive scan over the 256 threads of a block; *total gets the sum.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* total) {
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    int inc = v;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int n = __shfl_up(inc, off);
+        if (lane >= off) inc += n;
+    }
+    if (lane == kWave - 1) wsum[wave] = inc;
+    __syncthreads();
+    int before = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerChunk; ++w) {
+        if (w < wave) before += wsum[w];
+        all += wsum[w];
+    }
+    __syncthreads();
+    *total = all;
+    return before + inc - v;
+}
+
+// ---------------------------------------------------------------- 1. count
+__global__ __launch_bounds__(kChunk) void layout_count_kernel(
+    Geom g, const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep,
+    const uint64_t* __restrict__ mask, const int32_t* __restrict__ er, const int32_t* __restrict__ el,
+    Workspace ws, uint8_t* __restrict__ vol) {
+    // one partial row per chunk (sub == 1)
+    __shared__ int cnt[kMaxW];
+    __shared__ int pos_lds[kMaxE];
+    __shared__ int vsum[kWavesPerChunk][4];
+    for (int i = threadIdx.x; i < g.W; i += blockDim.x) cnt[i] = 0;
+    for (int e = threadIdx.x; e < g.E; e += blockDim.x) pos_lds[e] = slot_position(er, el, e, g);
+    __syncthreads();
+
+    int t0, t1, src;
+    chunk_range(g, blockIdx.x, t0, t1, src);
+    const int t = t0 + threadIdx.x;
+    int v[4] = {0, 0, 0, 0};       // n_dev, n_intra_remote, n_inter, n_nodes
+    if (t < t1) {
+        int P[kMaxK];
+        uint64_t m;
+        load_token(g, t, idx, keep, mask, pos_lds, P, m);
+#pragma unroll
+        for (int s = 0; s < kMaxK; ++s)
+            if (P[s] >= 0) atomicAdd(&cnt[P[s]], 1);
+        const int src_node = src / g.rpn;
+        uint64_t nodes = 0;
+        for (uint64_t b = m; b; b &= b - 1) {
+            const int d = __ffsll(static_cast<unsigned long long>(b)) - 1;
+            atomicAdd(&cnt[g.E + d], 1);
+            ++v[0];
+            const int nd = d / g.rpn;
+            if (nd != src_node) ++v[2];
+            else if (d != src) ++v[1];
+            nodes |= 1ull << nd;
+        }
+        v[3] = __popcll(nodes);
+        reinterpret_cast<uint32_t*>(vol)[t] = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 8) |
+                                              (static_cast<uint32_t>(v[2]) << 16) | (static_cast<uint32_t>(v[3]) << 24);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int s = wave_sum(v[j]);
+        if (lane_id() == 0) vsum[threadIdx.x / kWave][j] = s;
+    }
+    __syncthreads();
+    int32_t* out = ws.part + static_cast<size_t>(blockIdx.x) * g.W;
+    for (int i = threadIdx.x; i < g.W; i += blockDim.x) out[i] = cnt[i];
+    if (threadIdx.x < 4) {
+        int64_t s = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerChunk; ++w) s += vsum[w][threadIdx.x];
+        ws.volpart[blockIdx.x * 4 + threadIdx.x] = s;
+    }
+}
+
+// ---------------------------------------------------------------- 2. colscan
+constexpr int kScanBatch = 8;
+
+// Column scan, block bid of g.W + 1: one block per column scans it over the
+// Cs partial rows (in place: counts -> exclusive bases) and writes its total;
+// block g.W sums the volumes.
+__device__ __forceinline__ void layout_colscan_block(const Geom& g, const Workspace& ws, int64_t* __restrict__ totals,
+                                                     int bid) {
+    __shared__ int wsum[kWavesPerChunk];
+    if (bid == g.W) {
+        // volume totals: wave j sums column j of volpart
+        const int j = threadIdx.x / kWave;
+        int64_t s = 0;
+        for (int c = lane_id(); c < g.Cs; c += kWave) s += ws.volpart[c * 4 + j];
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+        if (lane_id() == 0) totals[j] = s;
+        return;
+    }
+    const int col = bid;
+    const int per = (g.Cs + kChunk - 1) / kChunk;         // partial rows per thread, consecutive
+    const int c0 = min(g.Cs, static_cast<int>(threadIdx.x) * per);
+    const int c1 = min(g.Cs, c0 + per);
+    int mine = 0;
+    for (int b = c0; b < c1; b += kScanBatch) {
+        int x[kScanBatch];
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) mine += x[i];
+    }
+    int total;
+    int run = block_exclusive_scan(mine, wsum, &total);
+    for (int b = c0; b < c1; b += kScanBatch) {
+        int x[kScanBatch];
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) {
+            if (b + i < c1) ws.part[static_cast<size_t>(b + i) * g.W + col] = run;
+            run += x[i];
+        }
+    }
+    if (threadIdx.x == 0) ws.coltot[col] = total;
+}
+
+__global__ __launch_bounds__(kChunk) void layout_colscan_kernel(Geom g, Workspace ws, int64_t* __restrict__ totals) {
+    layout_colscan_block(g, ws, totals, blockIdx.x);
+}
+
+// ---------------------------------------------------------------- 3. scatter
+// Scatter of chunk bid (one block of kChunk threads per chunk).
+__device__ __forceinline__ void layout_scatter_block(
+    const Geom& g, const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep,
+    const uint64_t* __restrict__ mask, const int32_t* __restrict__ er, const int32_t* __restrict__ el,
+    const Workspace& ws, int32_t* __restrict__ send_counts, int32_t* __restrict__ send_offsets,
+    int32_t* __restrict__ recv_offsets, int32_t* __restrict__ expert_counts,
+    int32_t* __restrict__ expert_offsets, int32_t* __restrict__ slot_pos,
+    int32_t* __restrict__ copy_row, int32_t* __restrict__ recv_token, int bid) {
+    __shared__ unsigned long long bits[kWavesPerChunk][kMaxW];
+    __shared__ int32_t pre[kWavesPerChunk][kMaxW];
+    __shared__ int pos_lds[kMaxE];
+    __shared__ int32_t gbase[kMaxW];
+    __shared__ int32_t roff[kMaxR + 1];
+    __shared__ int wsum[kWavesPerChunk];
+    const int wave = threadIdx.x / kWave;
+    for (int i = threadIdx.x; i < kWavesPerChunk * g.W; i += blockDim.x) bits[i / g.W][i % g.W] = 0ull;
+    for (int e = threadIdx.x; e < g.E; e += blockDim.x) pos_lds[e] = slot_position(er, el, e, g);
+
+    // expert offsets (slot-position order) and receive offsets from the column totals
+    const int32_t* cb = ws.part + static_cast<size_t>(bid) * g.sub * g.W;     // the chunk's first partial row
+    {
+        const int i = threadIdx.x;              // E <= 256 = blockDim.x
+        const int tot_e = i < g.E ? ws.coltot[i] : 0;
+        int rows_total;
+        const int eoff = block_exclusive_scan(tot_e, wsum, &rows_total);
+        const int tot_d = i < g.R ? ws.coltot[g.E + i] : 0;
+        int recv_total;
+        const int doff = block_exclusive_scan(tot_d, wsum, &recv_total);
+        if (i < g.E) gbase[i] = cb[i] + eoff;
+        if (i < g.R) {
+            gbase[g.E + i] = cb[g.E + i];
+            roff[i] = doff;
+        }
+        if (i == 0) roff[g.R] = recv_total;
+        if (bid == 0) {
+            if (i < g.E) {
+                expert_counts[i] = tot_e;
+                expert_offsets[i] = eoff;
+            }
+            if (i == 0) expert_offsets[g.E] = rows_total;
+            if (i < g.R) recv_offsets[i] = doff;
+            if (i == 0) recv_offsets[g.R] = recv_total;
+            // send_counts[s][d] = rows of d from chunks of rank s
+            if (i < g.R) {
+                const int s = i;
+                int run = 0;
+                for (int d = 0; d < g.R; ++d) {
+                    const int lo = ws.part[static_cast<size_t>(s * g.cpr * g.sub) * g.W + g.E + d];
+                    const int hi = (s + 1 < g.R)
+                                       ? ws.part[static_cast<size_t>((s + 1) * g.cpr * g.sub) * g.W + g.E + d]
+                                       : ws.coltot[g.E + d];
+                    send_counts[s * g.R + d] = hi - lo;
+                    send_offsets[s * g.R + d] = run;
+                    run += hi - lo;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    int t0, t1, src;
+    chunk_range(g, bid, t0, t1, src);
+    const int t = t0 + threadIdx.x;
+    const bool live = t < t1;
+    const unsigned long long me = 1ull << lane_id();
+    int P[kMaxK];
+    uint64_t m = 0;
+    if (live) {
+        load_token(g, t, idx, keep, mask, pos_lds, P, m);
+#pragma unroll
+        for (int s = 0; s < kMaxK; ++s)
+            if (P[s] >= 0) atomicOr(&bits[wave][P[s]], me);
+        for (uint64_t b = m; b; b &= b - 1)
+            atomicOr(&bits[wave][g.E + __ffsll(static_cast<unsigned long long>(b)) - 1], me);
+    }
+    __syncthreads();
+    for (int col = threadIdx.x; col < g.W; col += blockDim.x) {
+        int run = 0;
+#pragma unroll
+        for (int w = 0; w < kWavesPerChunk; ++w) {
+            pre[w][col] = run;
+            run += __popcll(bits[w][col]);
+        }
+    }
+    __syncthreads();
+    if (!live) return;
+    const unsigned long long below = lanemask_lt();
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s) {
+        if (s >= g.k) break;
+        const size_t q = static_cast<size_t>(t) * g.k + s;
+        int sp = -1, cr = -1;
+        if (P[s] >= 0) {
+            const int Pe = P[s];
+            sp = gbase[Pe] + pre[wave][Pe] + __popcll(bits[wave][Pe] & below);
+            const int d = Pe / g.E_loc;
+            const int col = g.E + d;
+            if ((m >> d) & 1ull) cr = gbase[col] + pre[wave][col] + __popcll(bits[wave][col] & below);
+        }
+        slot_pos[q] = sp;
+        copy_row[q] = cr;
+    }
+    for (uint64_t b = m; b; b &= b - 1) {
+        const int d = __ffsll(static_cast<unsigned long long>(b)) - 1;
+        const int col = g.E + d;
+        const int row = gbase[col] + pre[wave][col] + __popcll(bits[wave][col] & below);
+        const long long at = static_cast<long long>(roff[d]) + row;
+        if (at >= 0 && at < static_cast<long long>(g.T) * g.k) recv_token[at] = t;   // malformed masks stay in bounds
+    }
+}
+
+__global__ __launch_bounds__(kChunk) void layout_scatter_kernel(
+    Geom g, const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep,
+    const uint64_t* __restrict__ mask, const int32_t* __restrict__ er, const int32_t* __restrict__ el,
+    Workspace ws, int32_t* __restrict__ send_counts, int32_t* __restrict__ send_offsets,
+    int32_t* __restrict__ recv_offsets, int32_t* __restrict__ expert_counts,
+    int32_t* __restrict__ expert_offsets, int32_t* __restrict__ slot_pos,
+    int32_t* __restrict__ copy_row, int32_t* __restrict__ recv_token) {
+    layout_scatter_block(g, idx, keep, mask, er, el, ws, send_counts, send_offsets, recv_offsets, expert_counts,
+                         expert_offsets, slot_pos, copy_row, recv_token, blockIdx.x);
+}
+
+inline Geom make_geom(const cap_topology* tp, int sub) {
+    Geom g;
+    g.T = tp->T; g.E = tp->E; g.k = tp->k; g.R = tp->R; g.rpn = tp->ranks_per_node;
+    g.tpr = tp->tokens_per_rank; g.E_loc = tp->E / tp->R;
+    g.cpr = (tp->tokens_per_rank + kChunk - 1) / kChunk;
+    g.C = g.R * g.cpr;
+    g.W = g.E + g.R;
+    g.sub = sub;
+    g.Cs = g.C * sub;
+    return g;
+}
+
+inline Workspace carve(const Geom& g, void* base, size_t* bytes) {
+    char* p = static_cast<char*>(base);
+    Workspace w;
+    size_t off = 0;
+    w.part = reinterpret_cast<int32_t*>(p + off);
+    off += align256(static_cast<size_t>(g.Cs) * g.W * sizeof(int32_t));
+    w.coltot = reinterpret_cast<int32_t*>(p + off);
+    off += align256(static_cast<size_t>(g.W) * sizeof(int32_t));
+    w.volpart = reinterpret_cast<int64_t*>(p + off);
+    off += static_cast<size_t>(g.Cs) * 4 * sizeof(int64_t);
+    if (bytes) *bytes = off;
+    return w;
+}
+
+}  // namespace
+}  // namespace cap

@@ -144,16 +144,25 @@ __device__ __forceinline__ void lane_cx(double& key, float& a, bool lower) {
 }
 constexpr int kDppMirror4 = 0x1B;       // quad_perm [3,2,1,0]
 
+// What a lane knows of its token after the decision: the expert of its slot
+// (lane g < K), whether that slot is kept, and the token's device mask.
+struct RouteResult {
+    int e;
+    bool has_slot, keep;
+    uint64_t mask;
+};
+
 // The whole decision for one token, from its logits: lane g (of the token's
 // 8-lane group) holds vals[c * CW + i] = logit of expert c * (8 * CW) + g * CW
 // + i, CW = min(V, 4).  er_lds[e] is the rank of expert e (LDS, ready).
-// Writes idx / w' / keep for slot g (g < K) and the device mask (lane 0).
+// Writes idx / w' / keep for slot g (g < K) and the device mask (lane 0), and
+// returns the lane's part of the result.
 template <int V, int K, bool VEC, bool NAIVE>
-__device__ __forceinline__ void route_token(const float (&vals)[V], int g, int t, bool live, int E, int R,
-                                            int ranks_per_node, int tokens_per_rank, float inter_node_cost,
-                                            float p, const int* er_lds, int32_t* __restrict__ out_idx,
-                                            float* __restrict__ out_w, uint8_t* __restrict__ out_keep,
-                                            uint64_t* __restrict__ out_mask) {
+__device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g, int t, bool live, int E, int R,
+                                                   int ranks_per_node, int tokens_per_rank, float inter_node_cost,
+                                                   float p, const int* er_lds, int32_t* __restrict__ out_idx,
+                                                   float* __restrict__ out_w, uint8_t* __restrict__ out_keep,
+                                                   uint64_t* __restrict__ out_mask) {
     constexpr int KP = pow2_at_least(K);
     constexpr int CW = V < 4 ? V : 4;
     double keys[V];
@@ -281,17 +290,18 @@ __device__ __forceinline__ void route_token(const float (&vals)[V], int g, int t
     }
 
     // ---- lane g writes slot g
+    const bool my_keep = has_slot && (NAIVE ? (g < n_keep) : ((mask >> (my_dev & 63)) & 1ull));
     if (live && has_slot) {
         float my_w = ws[0];
 #pragma unroll
         for (int s = 1; s < K; ++s) my_w = (g == s) ? ws[s] : my_w;
-        const bool my_keep = NAIVE ? (g < n_keep) : ((mask >> my_dev) & 1ull);
         const size_t qi = static_cast<size_t>(t) * K + g;
         out_idx[qi] = my_e;
         out_w[qi] = my_keep ? my_w / Sk : 0.0f;
         out_keep[qi] = my_keep ? 1 : 0;
         if (g == 0) out_mask[t] = mask;
     }
+    return RouteResult{my_e, has_slot, my_keep, mask};
 }
 
 }  // namespace

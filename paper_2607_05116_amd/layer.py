@@ -70,6 +70,8 @@ class DeviceLayer:
         self.ws_layout = self._ws(capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, self.topo))
         self.coact = torch.zeros((E, E), dtype=torch.int32, device=self.dev)
         self.ws_coact = self._ws(capi.cap_workspace_size(capi.CAP_OP_COACTIVATION, self.topo))
+        self.ws_front = self._ws(capi.cap_workspace_size(capi.CAP_OP_ROUTE_LAYOUT, self.topo))
+        self.fused_front = True         # routing, layout and co-activation in three launches (CAP pruning)
         # rank-side buffers
         self.row_cap = row_cap if row_cap is not None else T * min(k, cfg.E_loc)
         self.recv_cap = recv_cap if recv_cap is not None else T * min(k, R)
@@ -123,6 +125,12 @@ class DeviceLayer:
         """Router GEMM x W_g^T fused with top-k routing and pruning (bf16 x)."""
         capi.cap_router_route_prune(self.topo, self.dt, self.d, self.x, w_gate, self.p, self.idx, self.w,
                                     self.keep, self.mask, logits_out, stream)
+
+    def route_layout(self, coactivation=True, stream=None):
+        """Routing, pruning, layout and (optionally) co-activation counts in
+        the fused three-launch front end."""
+        capi.cap_route_layout(self.topo, self.logits, self.p, self.idx, self.w, self.keep, self.mask, self.lay,
+                              self.coact if coactivation else None, self.ws_front, stream=stream)
 
     def layout(self, stream=None):
         capi.cap_dispatch_layout(self.topo, self.idx, self.keep, self.mask, self.lay, self.ws_layout,
@@ -181,15 +189,21 @@ class DeviceLayer:
                          self.y.shape[0], stream)
 
     def front(self, stream=None, side=None):
-        """Routing front end over all virtual ranks' tokens.  With a side
-        stream, the co-activation counts (which only feed placement) run there
-        beside the layout; the main stream waits for them before returning
-        control to later work."""
-        self.route(stream)
+        """Routing front end over all virtual ranks' tokens: the fused
+        three-launch front end (CAP pruning), or route, layout and
+        co-activation as separate calls (naive pruning, or fused_front off).
+        In the separate form, with a side stream the co-activation counts
+        (which only feed placement) run there beside the layout; the main
+        stream waits for them before returning control to later work."""
+        if self.fused_front and not self.naive:
+            self.route_layout(True, stream)
+            return
         if side is None:
+            self.route(stream)
             self.layout(stream)
             self.coactivation(False, stream)
             return
+        self.route(stream)
         main = stream if stream is not None else torch.cuda.current_stream()
         if not hasattr(self, "_fork"):
             self._fork, self._join = torch.cuda.Event(), torch.cuda.Event()
@@ -248,7 +262,20 @@ class DeviceLayer:
         is done; the main stream joins it before the source reduce, which adds
         the shared output.  ffn_events: as in rank_path."""
         main = stream if stream is not None else torch.cuda.current_stream()
-        if side is None:
+        if side is None or (self.fused_front and not self.naive):
+            # the fused front end, then (beside it on the side stream, when
+            # there is one) the shared experts, which read only x
+            if side is not None:
+                if not hasattr(self, "_step_ev"):
+                    self._step_ev = [torch.cuda.Event() for _ in range(3)]
+                start, _, side_done = self._step_ev
+                start.record(main)
+                side.wait_event(start)
+                self.shared_ffn(rank, side)
+                side_done.record(side)
+                self.front(main)
+                self.rank_path(rank, main, ffn_events, join=side_done)
+                return
             self.front(main)
             self.rank_path(rank, main, ffn_events)
             return

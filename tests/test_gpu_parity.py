@@ -57,6 +57,64 @@ def test_route_layout_coact_bit_exact(case):
 
 
 @pytest.mark.parametrize("case", C.ROUTE_CASES, ids=lambda c: c.id)
+def test_route_layout_fused_bit_exact(case):
+    """cap_route_layout (routing, layout and co-activation in three launches)
+    gives the oracle's routing, layout, volumes and co-activation bit for bit,
+    and the separate calls' bits; without a co-activation output it leaves
+    the counts alone."""
+    L = _layer(case, row_cap=8, recv_cap=8)
+    L.coact.fill_(-1)
+    L.route_layout(True)
+    torch.cuda.synchronize()
+    r, lay = C.oracle_routing(case.name, case.placement, case.p, case.c)
+    assert np.array_equal(L.host("idx"), r["idx"])
+    assert np.array_equal(L.host("w").view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(L.host("keep"), r["keep"])
+    assert np.array_equal(L.host("mask").view(np.uint64), r["mask"])
+    for name in ("send_counts", "send_offsets", "recv_offsets", "expert_counts", "expert_offsets",
+                 "slot_pos", "copy_row", "vol", "totals"):
+        assert np.array_equal(L.host(name), lay[name]), name
+    n_recv = int(lay["recv_offsets"][-1])
+    assert np.array_equal(L.host("recv_token")[:n_recv], lay["recv_token"])
+    coact = oracle.coactivation(r["idx"], r["keep"], case.cfg.E)
+    assert np.array_equal(L.host("coact").view(np.uint32), coact)
+    L.coact.fill_(7)
+    L.route_layout(False)
+    torch.cuda.synchronize()
+    assert int((L.coact != 7).sum()) == 0
+    assert np.array_equal(L.host("slot_pos"), lay["slot_pos"])
+
+
+@pytest.mark.parametrize("E,k,R,rpn,p,c,T_loc", [
+    (16, 2, 4, 4, 0.3, 5.0, 160), (64, 6, 8, 4, 0.25, 5.0, 300), (128, 8, 16, 8, 0.1, 5.0, 129),
+    (256, 8, 32, 8, 0.2, 3.0, 97), (7, 3, 1, 1, 0.4, 5.0, 1000), (24, 5, 6, 2, 0.5, 2.0, 256),
+    (128, 8, 64, 8, 0.3, 5.0, 64), (96, 1, 8, 8, 0.0, 5.0, 385), (40, 8, 4, 2, 0.05, 5.0, 1)])
+def test_route_layout_fused_odd_shapes(E, k, R, rpn, p, c, T_loc):
+    """The fused front end on adversarial logits (ties, +-0) and ragged token
+    counts per rank (empty and partial 32-token parts), against the oracle."""
+    T = R * T_loc
+    L0 = _adversarial_logits(T, E, E + k + T_loc)
+    perm = np.random.default_rng(R + T_loc).permutation(E)
+    er, el = (perm // (E // R)).astype(np.int32), (perm % (E // R)).astype(np.int32)
+    cfg = gen.Config("adv", T=T, d=8, E=E, k=k, inter=128, R=R, ranks_per_node=rpn, n_clusters=1,
+                     zipf_s=0.0, dtype="bf16")
+    Ld = DeviceLayer(cfg, L0, np.zeros((T, 8), np.uint16), er, el, p, c, row_cap=8, recv_cap=8)
+    Ld.route_layout(True)
+    torch.cuda.synchronize()
+    r = oracle.route_prune(L0, k, er, rpn, T // R, c, p)
+    lay = oracle.dispatch_layout(r["idx"], r["keep"], r["mask"], er, el, R, rpn, T // R, E)
+    assert np.array_equal(Ld.host("idx"), r["idx"])
+    assert np.array_equal(Ld.host("w").view(np.uint32), r["wp"].view(np.uint32))
+    assert np.array_equal(Ld.host("mask").view(np.uint64), r["mask"])
+    for name in ("slot_pos", "copy_row", "vol", "expert_offsets", "expert_counts", "send_counts",
+                 "send_offsets", "recv_offsets", "totals"):
+        assert np.array_equal(Ld.host(name), lay[name]), name
+    n_recv = int(lay["recv_offsets"][-1])
+    assert np.array_equal(Ld.host("recv_token")[:n_recv], lay["recv_token"])
+    assert np.array_equal(Ld.host("coact").view(np.uint32), oracle.coactivation(r["idx"], r["keep"], E))
+
+
+@pytest.mark.parametrize("case", C.ROUTE_CASES, ids=lambda c: c.id)
 def test_naive_pruning_bit_exact(case):
     """Expert-level threshold pruning (the comparison baseline) against the
     oracle: routing outputs and the layout built from them."""

@@ -194,3 +194,20 @@ def test_adjustment_rejects_bad_arguments(capi, over):
     st = capi._lib.cap_adjustment_spectrum(0x1000, 16, 4, 2, 5.0, 0x2000, 0x3000, 4, 0x4000, None, 0x5000,
                                            0x6000, 16 * 16 * 8 - 1, None)
     assert st == capi.CAP_ERR_WORKSPACE
+
+
+def test_route_layout_validation(capi):
+    """The fused front end validates like the separate calls, and sizes its
+    workspace for eight count rows per 256-token chunk plus co-activation."""
+    t = _topo(capi, E=128, R=8, ranks_per_node=8, T=32768, k=8)
+    need = capi.cap_workspace_size(capi.CAP_OP_ROUTE_LAYOUT, t)
+    assert need > capi.cap_workspace_size(capi.CAP_OP_DISPATCH_LAYOUT, t)
+    lay = capi.Layout(*([0x9000] * 10))
+    f = capi._lib.cap_route_layout
+    assert f(ctypes.byref(t), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, ctypes.byref(lay), None, 0x10000,
+             need - 1, None) == capi.CAP_ERR_WORKSPACE
+    assert f(ctypes.byref(t), 0x3000, 1.0, 0x4000, 0x5000, 0x6000, 0x7000, ctypes.byref(lay), None, 0x10000,
+             need, None) == capi.CAP_ERR_INVALID_ARG
+    bad = _topo(capi, k=0)
+    assert f(ctypes.byref(bad), 0x3000, 0.3, 0x4000, 0x5000, 0x6000, 0x7000, ctypes.byref(lay), None, 0x10000,
+             need, None) == capi.CAP_ERR_INVALID_ARG
