@@ -154,7 +154,7 @@ def trace_logits(cfg: Config, seed: int = 0) -> np.ndarray:
     """fp32 logits [trace_tokens][E] of an independent batch from the same model.
 
     This is the routing trace that feeds co-activation placement (the paper
-    collects about 8,000 tokens offline before placing experts, Sec. VIII-F)."""
+    collects about 8,000 tokens offline before placing experts, Sec. VIII-G)."""
     a, b = _streams(seed)[_S_TRACE].spawn(2)
     return _latent_topic_logits(cfg, seed, cfg.trace_tokens, a, b)
 
