@@ -195,38 +195,102 @@ static_assert(kBM % (kRowsPerLoad * kNL) == 0 && kBN % (kRowsPerLoad * kNL) == 0
 static_assert(kALd + kBLd <= 60, "loads per stage must fit the vmcnt field");
 static_assert(kWN % 64 == 0, "gate/up pairs need 64-column wave tiles");
 static_assert(kBRun * kRowsPerLoad == 32, "a gate/up loader covers one 32-row W1/W3 pair");
+static_assert(kALd * kRowsPerLoad == kWM, "loader wave w loads the A rows that waves of row w read");
 static_assert(kStageK % 32 == 0, "fragments are read two K steps at a time");
 static_assert(kStages == 2, "staging lives in stage buffer 1");
 
-// One stage of a wave's MFMA work: its 64 x 128 block over the stage's K = 64,
-// fragments read from LDS two K steps at a time.  The MFMA takes the weight
-// fragment as its first operand, so a lane's 16 accumulators hold 4
-// consecutive output columns per register group.
-__device__ __forceinline__ void mma_stage(const uint8_t* sa, const uint8_t* sb, int wm, int wn, int fr_row,
-                                          int fr_swz, int fr_half, f32x16 (&acc)[kMI][kNJ]) {
-    constexpr int KS = kStageK / 16;                  // MFMA K steps per stage
+// Per-lane constants of the direct loads and the fragment reads.
+struct LaneMap {
+    int ld_row;          // direct loads: lane l writes row l / 8 of its 1 KiB block ...
+    uint32_t col_b[2];   // ... at physical chunk l % 8, fetching logical chunk (l % 8) ^ swz(row):
+                         // the swizzle of row (8 * blk + l / 8) is swz(l / 8) ^ (blk & 1)
+    int fr_row, fr_swz, fr_half;   // fragment reads: row r = ... + lane % 32, K half lane / 32
+};
+__device__ __forceinline__ LaneMap lane_map(int lane) {
+    LaneMap m;
+    m.ld_row = lane >> 3;
+    const int pc = lane & (kChunks - 1);
+    m.col_b[0] = static_cast<uint32_t>((pc ^ lds_swz(m.ld_row)) * 16);
+    m.col_b[1] = static_cast<uint32_t>((pc ^ lds_swz(kRowsPerLoad + m.ld_row)) * 16);
+    m.fr_row = lane & 31;
+    m.fr_swz = lds_swz(m.fr_row);
+    m.fr_half = lane >> 5;
+    return m;
+}
+
+// Fragments of one MFMA K step (K = 16) of a wave's 64 x 128 block: kMI A
+// fragments and kNJ B fragments, one 16-byte LDS read each.  Lane (r, h) =
+// (lane % 32, lane / 32) reads row r of each 32-row block, K half h.
+struct Frags {
+    bf16x8 a[kMI], b[kNJ];
+};
+
+__device__ __forceinline__ void read_frags(const uint8_t* st, int ks, int wm, int wn, int fr_row, int fr_swz,
+                                           int fr_half, Frags& f) {
+    const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
+    const uint8_t* sb = st + kBM * kRowB;
 #pragma unroll
-    for (int k2 = 0; k2 < KS; k2 += 2) {
-        bf16x8 fa[2][kMI], fb[2][kNJ];
+    for (int i = 0; i < kMI; ++i)
+        f.a[i] = *reinterpret_cast<const bf16x8*>(st + (wm * kWM + i * 32 + fr_row) * kRowB + pc);
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const int pc = ((2 * (k2 + ks) + fr_half) ^ fr_swz) << 4;
+    for (int j = 0; j < kNJ; ++j)
+        f.b[j] = *reinterpret_cast<const bf16x8*>(sb + (wn * kWN + j * 32 + fr_row) * kRowB + pc);
+}
+
+// The MFMAs of one K step.  The MFMA takes the weight fragment as its first
+// operand, so a lane's 16 accumulators hold 4 consecutive output columns per
+// register group.
+__device__ __forceinline__ void mma_frags(const Frags& f, f32x16 (&acc)[kMI][kNJ]) {
 #pragma unroll
-            for (int i = 0; i < kMI; ++i)
-                fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + (wm * kWM + i * 32 + fr_row) * kRowB + pc);
+    for (int i = 0; i < kMI; ++i)
 #pragma unroll
-            for (int j = 0; j < kNJ; ++j)
-                fb[ks][j] = *reinterpret_cast<const bf16x8*>(sb + (wn * kWN + j * 32 + fr_row) * kRowB + pc);
+        for (int j = 0; j < kNJ; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
+}
+
+// The MFMAs of the current K step with the fragment reads of the next one
+// (K step ks of the stage at st) issued between them, so that the LDS latency
+// of the next step hides behind this step's MFMAs.
+__device__ __forceinline__ void mma_and_read(const Frags& cur, f32x16 (&acc)[kMI][kNJ], const uint8_t* st, int ks,
+                                             int wm, int wn, int fr_row, int fr_swz, int fr_half, Frags& nxt) {
+    read_frags(st, ks, wm, wn, fr_row, fr_swz, fr_half, nxt);
+    mma_frags(cur, acc);
+    static_for<kMI + kNJ>([&](auto) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+    });
+    __builtin_amdgcn_sched_group_barrier(0x008, kMI * kNJ - (kMI + kNJ), 0);
+}
+
+// The K loop of one tile: KT stages of K = 64 (four K steps each).
+// sync(kt) makes stage kt visible and issues the loads of stage kt + 1 (the
+// loaders' wait for their own loads, the workgroup barrier, the next issue and
+// any per-stage bookkeeping of the caller).  A wave's fragment reads run one K
+// step ahead of its MFMAs; the barrier of stage kt + 1 comes after the reads of
+// stage kt's last K step have returned (so the loads issued after it may
+// overwrite stage kt's buffer) and before that step's MFMAs.  A wave whose
+// 64 rows all lie past the tile's valid rows (active = false) computes
+// nothing: its accumulators stay zero and are never stored.
+template <typename Sync>
+__device__ __forceinline__ void k_loop(int KT, const uint8_t* lds, int wm, int wn, const LaneMap& lm, bool active,
+                                       f32x16 (&acc)[kMI][kNJ], Sync&& sync) {
+    Frags f0, f1;
+    sync(0);
+    if (active) read_frags(lds, 0, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f0);
+    for (int kt = 0; kt < KT; ++kt) {
+        const uint8_t* st = lds + (kt % kStages) * kStageBytes;
+        if (active) {
+            mma_and_read(f0, acc, st, 1, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f1);
+            mma_and_read(f1, acc, st, 2, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f0);
+            mma_and_read(f0, acc, st, 3, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f1);
         }
-#pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
-#pragma unroll
-            for (int i = 0; i < kMI; ++i)
-#pragma unroll
-                for (int j = 0; j < kNJ; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ks][j], fa[ks][i], acc[i][j], 0, 0, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * (kMI + kNJ), 0);   // DS reads
-        __builtin_amdgcn_sched_group_barrier(0x008, 2 * kMI * kNJ, 0);     // MFMA
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");       // stage kt fully read
+        // stage kt + 1 visible (after the last stage: a plain barrier; the
+        // fragments read after it are never used)
+        sync(kt + 1);
+        if (active)
+            mma_and_read(f1, acc, lds + ((kt + 1) % kStages) * kStageBytes, 0, wm, wn, lm.fr_row, lm.fr_swz,
+                         lm.fr_half, f0);
     }
 }
 
@@ -320,25 +384,6 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
     }
 }
 
-// Per-lane constants of the direct loads and the fragment reads.
-struct LaneMap {
-    int ld_row;          // direct loads: lane l writes row l / 8 of its 1 KiB block ...
-    uint32_t col_b[2];   // ... at physical chunk l % 8, fetching logical chunk (l % 8) ^ swz(row):
-                         // the swizzle of row (8 * blk + l / 8) is swz(l / 8) ^ (blk & 1)
-    int fr_row, fr_swz, fr_half;   // fragment reads: row r = ... + lane % 32, K half lane / 32
-};
-__device__ __forceinline__ LaneMap lane_map(int lane) {
-    LaneMap m;
-    m.ld_row = lane >> 3;
-    const int pc = lane & (kChunks - 1);
-    m.col_b[0] = static_cast<uint32_t>((pc ^ lds_swz(m.ld_row)) * 16);
-    m.col_b[1] = static_cast<uint32_t>((pc ^ lds_swz(kRowsPerLoad + m.ld_row)) * 16);
-    m.fr_row = lane & 31;
-    m.fr_swz = lds_swz(m.fr_row);
-    m.fr_half = lane >> 5;
-    return m;
-}
-
 // Operand sources of one tile for one loader wave: A rows (or, gathered, the
 // base of x) and the wave's two 32-row B runs; pitch = bytes per operand row.
 struct TileSrc {
@@ -358,7 +403,10 @@ __device__ __forceinline__ void issue_stage(const TileSrc& s, int kt, int wave, 
     const uint32_t kb = static_cast<uint32_t>(kt) * kStageK * 2;
     const uint32_t a_lds = st + wave * kALd * 1024;
     const int a_first = wave * kALd * kRowsPerLoad;
-    if (gathered) {
+    if (a_first >= s.rows) {
+        // no valid row in this wave's 64 A rows: the waves that would read them
+        // compute nothing (k_loop's active flag), so they are not loaded
+    } else if (gathered) {
         static_for<kALd>([&](auto I) { lds_dma16_at(s.a, a_off[I.value], kb, a_lds + I.value * 1024); });
     } else if (a_first + kALd * kRowsPerLoad <= s.rows) {                 // wave-uniform
         const char* a_base = s.a + kb + static_cast<size_t>(wave * kALd) * s.blk;
@@ -486,13 +534,11 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-        for (int kt = 0; kt < KT; ++kt) {
+        k_loop(KT, lds, wm, wn, lm, wm * kWM < rows, acc, [&](int kt) {
             if (loader) wait_loads();              // this wave's part of stage kt has landed
             block_barrier();                       // stage kt visible; the other buffer is free
             if (loader && kt + 1 < KT) issue_stage(src, kt + 1, wave, lm, lane_off, GATHER, a_off, lds_base);
-            const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
-            mma_stage(sa, sa + kBM * kRowB, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, acc);
-        }
+        });
 
         // every wave is done with this tile's LDS: loaders start the next
         // tile's stage 0 (buffer 0), buffer 1 becomes the staging area
@@ -690,7 +736,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
             const int KT = T.KT;
             const bool ahead = KT >= 4;            // claim, publish and poll inside the K loop
             int claim = 0, poll = 0;
-            for (int kt = 0; kt < KT; ++kt) {
+            k_loop(KT, lds, wm, wn, lm, wm * kWM < T.rows, acc, [&](int kt) {
                 if (loader) wait_loads();
                 block_barrier();
                 if (kt + 1 < KT) issue(kt + 1);
@@ -712,9 +758,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
                         }
                     }
                 }
-                const uint8_t* sa = lds + (kt % kStages) * kStageBytes;
-                mma_stage(sa, sa + kBM * kRowB, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, acc);
-            }
+            });
             if (ahead && wave == 0 && lane == 0) {
                 const int nx = bcast[0];
                 bcast[1] = (nx < GU || nx >= Q || poll >= target) ? 1 : 0;
