@@ -56,6 +56,9 @@ def parse():
                     help="time eager launches (default: the step captured once as a HIP graph, replayed)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--cpu-stride", type=int, default=4, help="oracle FFN runs every n-th rank-0 row")
+    ap.add_argument("--separate-combine", action="store_true",
+                    help="run the destination combine as its own kernel after the FFN (for comparison; default: "
+                         "single-expert tokens combined in the FFN's epilogue)")
     ap.add_argument("--quick", action="store_true",
                     help="only the timed step and its FFN timing (no stage times, cold-cache replays, "
                          "sweeps, spectrum, second workload): for profiler runs")
@@ -416,6 +419,8 @@ def main():
         args.p = DEFAULT_P[args.config]
     rank = args.rank
     L, logits, x, er, el, coact_counts = build_layer(cfg, args.placement, args.p, args.c, rank)
+    if args.separate_combine:
+        L.fused_combine = False
 
     stream = torch.cuda.current_stream()
     # a side stream for the shared experts and the co-activation counts when
@@ -425,8 +430,9 @@ def main():
 
     def one_step(ev=None):
         """The whole hot path once: front end over all tokens, then rank r's
-        row source, gathered FFN, destination reduce and source reduce, with
-        the shared experts and the co-activation counts on the side stream."""
+        row plan, gathered FFN (which writes single-expert tokens' weighted
+        rows into the receive buffer), destination reduce of the other tokens
+        and source reduce, with the shared experts on the side stream."""
         L.step(rank, side=side, ffn_events=ev)
 
     # the graph is captured first, so that the eager loop, the graph warmup
@@ -537,8 +543,11 @@ def main():
             "parallelism": "1 GPU, virtual EP ranks",
         },
         "roofline": {
-            "kernel": ("cap_expert_ffn_gather, rank 0: one fused gate/up + down launch reading x rows in place "
-                       "(the call's events also hold its one-block counter clear, a few us)"),
+            "kernel": (("cap_expert_ffn_combine" if L.fused_combine else "cap_expert_ffn_gather")
+                       + ", rank 0: one fused gate/up + down launch reading x rows in place"
+                       + (" and writing single-expert tokens' weighted rows into the receive buffer"
+                          if L.fused_combine else "")
+                       + " (the call's events also hold its one-block counter clear, a few us)"),
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
             "flops_per_call": flops, "rows": rows, "avg_call_ms": ffn_ms,
@@ -583,10 +592,11 @@ def detail_measurements(args, L, cfg, rank, stream, totals):
     # of 20 back-to-back calls (every stage rewrites the same buffers from
     # unchanged inputs) and replayed, so launch gaps do not enter the times
     stages = ["front_fused", "route", "layout", "coact", "row_source", "ffn", "dest", "shared", "src", "gather",
-              "ffn_rows"]
+              "ffn_rows", "row_plan", "ffn_combine", "dest_multi"]
     fns = [L.route_layout, L.route, L.layout, L.coactivation, lambda: L.row_source(rank), lambda: L.ffn_gather(rank),
            lambda: L.dest_reduce(rank), lambda: L.shared_ffn(rank), lambda: L.src_reduce(rank),
-           lambda: L.gather(rank), lambda: L.ffn(rank)]
+           lambda: L.gather(rank), lambda: L.ffn(rank), lambda: L.row_plan(rank), lambda: L.ffn_combine(rank),
+           lambda: L.dest_reduce_multi(rank)]
 
     def stage_time(fn, n=20, reps=5):
         cap = torch.cuda.Stream()
@@ -610,7 +620,8 @@ def detail_measurements(args, L, cfg, rank, stream, totals):
 
     stage_ms = {}
     for s_name, fn in zip(stages, fns):
-        if s_name == "shared" and not cfg.n_shared:
+        if (s_name == "shared" and not cfg.n_shared) or (s_name in ("row_plan", "ffn_combine", "dest_multi")
+                                                         and not L.fused_combine):
             stage_ms[s_name] = 0.0
             continue
         stage_ms[s_name] = round(stage_time(fn), 5)

@@ -63,7 +63,10 @@ typedef enum {
 
 typedef enum {
     CAP_COMBINE_DEST_REDUCE = 0, /* per received token: weighted sum of the rank's expert rows */
-    CAP_COMBINE_SRC_REDUCE = 1   /* per source token: sum of the returned rows (+ shared) */
+    CAP_COMBINE_SRC_REDUCE = 1,  /* per source token: sum of the returned rows (+ shared) */
+    /* DEST_REDUCE for the received tokens with two or more kept experts on the
+       rank only; the single-expert ones were written by cap_expert_ffn_combine */
+    CAP_COMBINE_DEST_REDUCE_MULTI = 2
 } cap_combine_mode;
 
 typedef enum {
@@ -384,6 +387,49 @@ cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t 
                              size_t ws_bytes, const cap_ffn_options *opt, void *stream);
 
 /*
+ * Row plan of rank r's expert-sorted rows for cap_expert_ffn_combine (Sec.
+ * II-C: the local aggregation of a received token is the weighted sum of its
+ * kept experts on the rank, Eq. 1; a token with a single kept expert there
+ * has a one-term sum, which the FFN's epilogue can write directly).  For every
+ * kept slot (t, s) on r, with row i = slot_pos(t,s) - expert_offsets[r*E_loc]
+ * < rows_cap and t the u-th token of r's receive buffer:
+ *   row_src[i] = t                       (as CAP_PERMUTE_ROW_SOURCE);
+ *   row_dst[i] = recv_offsets[r] + u     if t has no other kept slot whose
+ *                                        row on r is < rows_cap, and
+ *                                        recv_offsets[r] + u < parts_rows;
+ *                -1                      otherwise;
+ *   row_w[i]   = w'(t,s) where row_dst[i] >= 0, else 0.
+ * w is cap_route_prune's w'.  Rows with no kept slot are not written.  All
+ * arrays are device int32 / fp32 of rows_cap entries.  No workspace.
+ */
+cap_status cap_row_plan(const cap_topology *topo, int32_t rank, const float *w, const cap_layout *lay,
+                        int32_t *row_src, int32_t *row_dst, float *row_w, int32_t rows_cap,
+                        int32_t parts_rows, void *stream);
+
+/*
+ * cap_expert_ffn_ex (bf16) with the destination combine of single-expert
+ * tokens folded into the down GEMM's epilogue (Eq. 1; Sec. II-C local
+ * aggregation).  For each row i < max_rows:
+ *   0 <= row_dst[i] < parts_rows:  parts[row_dst[i]] = bf16(fmaf(row_w[i], y_i, 0))
+ *       with y_i = the bf16 FFN output row, the arithmetic CAP_COMBINE_DEST_REDUCE
+ *       does for a one-term sum, so the bits equal that path's; y[i] is not
+ *       written;
+ *   otherwise:                     y[i] as cap_expert_ffn_ex.
+ * row_dst, row_w: device int32 / fp32 [max_rows] (cap_row_plan); parts:
+ * [parts_rows][d] bf16, 16-byte aligned (the concatenated receive-side buffer
+ * of cap_combine).  The remaining tokens then take
+ * cap_combine(CAP_COMBINE_DEST_REDUCE_MULTI) with in_rows = the plan's rows_cap
+ * and out_rows = parts_rows.  Other arguments, workspace, limits and errors as
+ * cap_expert_ffn_ex; CAP_ERR_UNSUPPORTED for f32.
+ */
+cap_status cap_expert_ffn_combine(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                                  const void *x, int32_t x_rows, const int32_t *row_src,
+                                  const int32_t *row_offsets, const void *w1, const void *w3, const void *w2,
+                                  void *y, const int32_t *row_dst, const float *row_w, void *parts,
+                                  int32_t parts_rows, void *ws, size_t ws_bytes, const cap_ffn_options *opt,
+                                  void *stream);
+
+/*
  * Weighted combine (Sec. II-C local aggregation and final combination; Eq. 1).
  *   CAP_COMBINE_DEST_REDUCE, rank r: in = rank r's expert output rows (row order
  *       of CAP_PERMUTE_EXPERT_GATHER); for each row u < U_r of r's receive buffer,
@@ -391,6 +437,9 @@ cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t 
  *       out[recv_offsets[r] + u] = sum over kept slots s of t placed on r of
  *       w'_s * in[slot_pos(t,s) - expert_offsets[r*E_loc]].
  *       `out` is the concatenated receive-side buffer of all ranks.
+ *   CAP_COMBINE_DEST_REDUCE_MULTI: DEST_REDUCE for the tokens with two or more
+ *       kept slots whose rows on r are < in_rows; the others' out rows are left
+ *       as they are (cap_expert_ffn_combine writes them).
  *   CAP_COMBINE_SRC_REDUCE, rank s: in = that concatenated buffer (the rows each
  *       device returns); for each token t of s:
  *       out[t - s*tokens_per_rank] = sum over kept devices d of t (ascending) of

@@ -7,8 +7,8 @@ call raises CapError on a non-zero status.
 
 Function names follow the C ABI: cap_route_prune, cap_route_prune_naive, cap_router_route_prune,
 cap_dispatch_layout,
-cap_permute, cap_expert_ffn, cap_expert_ffn_gather, cap_expert_ffn_ex, cap_combine, cap_coactivation,
-cap_workspace_size, cap_status_string, cap_version.
+cap_permute, cap_row_plan, cap_expert_ffn, cap_expert_ffn_gather, cap_expert_ffn_ex, cap_expert_ffn_combine,
+cap_combine, cap_coactivation, cap_workspace_size, cap_status_string, cap_version.
 """
 from __future__ import annotations
 
@@ -23,7 +23,7 @@ LIB_PATH = os.path.join(_HERE, "libcap.so")
 CAP_OK, CAP_ERR_INVALID_ARG, CAP_ERR_UNSUPPORTED, CAP_ERR_WORKSPACE, CAP_ERR_HIP = 0, -1, -2, -3, -4
 CAP_DTYPE_F32, CAP_DTYPE_BF16 = 0, 1
 CAP_PERMUTE_EXPERT_GATHER, CAP_PERMUTE_SEND_PACK, CAP_PERMUTE_ROW_SOURCE = 0, 1, 2
-CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE = 0, 1
+CAP_COMBINE_DEST_REDUCE, CAP_COMBINE_SRC_REDUCE, CAP_COMBINE_DEST_REDUCE_MULTI = 0, 1, 2
 (CAP_OP_ROUTE_PRUNE, CAP_OP_DISPATCH_LAYOUT, CAP_OP_PERMUTE, CAP_OP_EXPERT_FFN,
  CAP_OP_COMBINE, CAP_OP_COACTIVATION, CAP_OP_ADJUSTMENT, CAP_OP_ROUTE_LAYOUT) = range(8)
 
@@ -31,7 +31,8 @@ EXPORTS = ["cap_status_string", "cap_version", "cap_workspace_size", "cap_route_
            "cap_router_route_prune",
            "cap_dispatch_layout", "cap_permute", "cap_expert_ffn", "cap_expert_ffn_gather", "cap_expert_ffn_ex",
            "cap_combine", "cap_coactivation", "cap_dispatch_layout_static",
-           "cap_dispatch_layout_static_max_bytes", "cap_adjustment_spectrum", "cap_route_layout"]
+           "cap_dispatch_layout_static_max_bytes", "cap_adjustment_spectrum", "cap_route_layout",
+           "cap_row_plan", "cap_expert_ffn_combine"]
 
 
 class CapError(RuntimeError):
@@ -84,6 +85,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                                    vp], ctypes.c_int),
         "cap_expert_ffn_ex": ([ctypes.c_int, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, sz,
                                P(FfnOptions), vp], ctypes.c_int),
+        "cap_expert_ffn_combine": ([ctypes.c_int, i32, i32, i32, i32, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp,
+                                    vp, i32, vp, sz, P(FfnOptions), vp], ctypes.c_int),
+        "cap_row_plan": ([P(Topology), i32, vp, P(Layout), vp, vp, vp, i32, i32, vp], ctypes.c_int),
         "cap_combine": ([P(Topology), ctypes.c_int, i32, ctypes.c_int, i32, vp, i32, vp, vp, vp, vp,
                          P(Layout), vp, vp, i32, vp], ctypes.c_int),
         "cap_coactivation": ([i32, i32, i32, vp, vp, vp, i32, vp, sz, vp], ctypes.c_int),
@@ -222,6 +226,22 @@ def cap_expert_ffn_ex(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_
         dtype, E_loc, d, inter, max_rows, _ptr(x), int(x_rows), _ptr(row_src), _ptr(row_offsets), _ptr(w1),
         _ptr(w3), _ptr(w2), _ptr(y), _ptr(ws), nbytes, ctypes.byref(options) if options is not None else None,
         _stream(stream)))
+
+
+def cap_expert_ffn_combine(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2, y,
+                           row_dst, row_w, parts, parts_rows, ws, ws_bytes=None, options: FfnOptions | None = None,
+                           stream=None):
+    nbytes = ws_bytes if ws_bytes is not None else ws.numel() * ws.element_size()
+    _check("cap_expert_ffn_combine", _lib.cap_expert_ffn_combine(
+        dtype, E_loc, d, inter, max_rows, _ptr(x), int(x_rows), _ptr(row_src), _ptr(row_offsets), _ptr(w1),
+        _ptr(w3), _ptr(w2), _ptr(y), _ptr(row_dst), _ptr(row_w), _ptr(parts), int(parts_rows), _ptr(ws), nbytes,
+        ctypes.byref(options) if options is not None else None, _stream(stream)))
+
+
+def cap_row_plan(topo, rank, w, layout: Layout, row_src, row_dst, row_w, rows_cap, parts_rows, stream=None):
+    _check("cap_row_plan", _lib.cap_row_plan(
+        ctypes.byref(topo), int(rank), _ptr(w), ctypes.byref(layout), _ptr(row_src), _ptr(row_dst), _ptr(row_w),
+        int(rows_cap), int(parts_rows), _stream(stream)))
 
 
 def cap_combine(topo, mode, rank, dtype, d, inp, in_rows, idx, w, keep, dst_mask, layout: Layout,

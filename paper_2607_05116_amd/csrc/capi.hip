@@ -25,7 +25,9 @@ size_t ffn_workspace_bytes(int, int, cap_dtype);
 cap_status ffn_supported(cap_dtype, int, int);
 cap_status expert_ffn_launch(cap_dtype, int, int, int, int, const void*, int, const int32_t*, const int32_t*,
                              const void*, const void*, const void*, void*, void*, const cap_ffn_options*,
-                             hipStream_t);
+                             hipStream_t, const int32_t*, const float*, void*, int);
+cap_status row_plan_launch(const cap_topology*, int, const float*, const cap_layout*, int32_t*, int32_t*, float*,
+                           int, int, hipStream_t);
 size_t coact_workspace_bytes(int, int);
 size_t adjustment_workspace_bytes(int);
 size_t front_end_workspace_bytes(const cap_topology*);
@@ -209,10 +211,15 @@ cap_status cap_permute(const cap_topology* topo, cap_permute_mode mode, int32_t 
                           as_stream(stream));
 }
 
-cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
-                             const void* x, int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets,
-                             const void* w1, const void* w3, const void* w2, void* y, void* ws, size_t ws_bytes,
-                             const cap_ffn_options* opt, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation shared by the FFN entry points (CAP_OK when the call may launch).
+cap_status ffn_check(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows, const void* x,
+                     int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets, const void* w1,
+                     const void* w3, const void* w2, void* y, void* ws, size_t ws_bytes,
+                     const cap_ffn_options* opt) {
     if (!x || !row_offsets || !w1 || !w3 || !w2 || !y) return CAP_ERR_INVALID_ARG;
     if (E_loc < 1 || E_loc > kMaxE || d < 1 || inter < 1 || max_rows < 0) return CAP_ERR_INVALID_ARG;
     if (row_src && x_rows < 1) return CAP_ERR_INVALID_ARG;
@@ -231,9 +238,51 @@ cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t 
     if (!aligned16(x) || !aligned16(y) || !aligned16(w1) || !aligned16(w3) || !aligned16(w2))
         return CAP_ERR_INVALID_ARG;
     if (!ws || ws_bytes < ffn_workspace_bytes(max_rows, inter, dtype) || !aligned16(ws)) return CAP_ERR_WORKSPACE;
+    return CAP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+cap_status cap_expert_ffn_ex(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                             const void* x, int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets,
+                             const void* w1, const void* w3, const void* w2, void* y, void* ws, size_t ws_bytes,
+                             const cap_ffn_options* opt, void* stream) {
+    const cap_status st = ffn_check(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2,
+                                    y, ws, ws_bytes, opt);
+    if (st != CAP_OK || max_rows == 0) return st;
+    return expert_ffn_launch(dtype, E_loc, d, inter, max_rows, x, row_src ? x_rows : 0, row_src, row_offsets, w1,
+                             w3, w2, y, ws, opt, as_stream(stream), nullptr, nullptr, nullptr, 0);
+}
+
+cap_status cap_expert_ffn_combine(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
+                                  const void* x, int32_t x_rows, const int32_t* row_src, const int32_t* row_offsets,
+                                  const void* w1, const void* w3, const void* w2, void* y, const int32_t* row_dst,
+                                  const float* row_w, void* parts, int32_t parts_rows, void* ws, size_t ws_bytes,
+                                  const cap_ffn_options* opt, void* stream) {
+    const cap_status st = ffn_check(dtype, E_loc, d, inter, max_rows, x, x_rows, row_src, row_offsets, w1, w3, w2,
+                                    y, ws, ws_bytes, opt);
+    if (st != CAP_OK) return st;
+    if (dtype != CAP_DTYPE_BF16) return CAP_ERR_UNSUPPORTED;
+    if (!row_dst || !row_w || !parts || parts_rows < 0) return CAP_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(row_dst) & 3) != 0 || (reinterpret_cast<uintptr_t>(row_w) & 3) != 0 ||
+        !aligned16(parts))
+        return CAP_ERR_INVALID_ARG;
     if (max_rows == 0) return CAP_OK;
     return expert_ffn_launch(dtype, E_loc, d, inter, max_rows, x, row_src ? x_rows : 0, row_src, row_offsets, w1,
-                             w3, w2, y, ws, opt, as_stream(stream));
+                             w3, w2, y, ws, opt, as_stream(stream), row_dst, row_w, parts, parts_rows);
+}
+
+cap_status cap_row_plan(const cap_topology* topo, int32_t rank, const float* w, const cap_layout* lay,
+                        int32_t* row_src, int32_t* row_dst, float* row_w, int32_t rows_cap, int32_t parts_rows,
+                        void* stream) {
+    if (!topo_ok(topo) || !w || !layout_ok(lay) || !row_src || !row_dst || !row_w) return CAP_ERR_INVALID_ARG;
+    if (rank < 0 || rank >= topo->R || rows_cap < 0 || parts_rows < 0) return CAP_ERR_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(row_src) & 3) != 0 || (reinterpret_cast<uintptr_t>(row_dst) & 3) != 0 ||
+        (reinterpret_cast<uintptr_t>(row_w) & 3) != 0)
+        return CAP_ERR_INVALID_ARG;
+    return row_plan_launch(topo, rank, w, lay, row_src, row_dst, row_w, rows_cap, parts_rows, as_stream(stream));
 }
 
 cap_status cap_expert_ffn(cap_dtype dtype, int32_t E_loc, int32_t d, int32_t inter, int32_t max_rows,
@@ -260,7 +309,7 @@ cap_status cap_combine(const cap_topology* topo, cap_combine_mode mode, int32_t 
     if (rank < 0 || rank >= topo->R || in_rows < 0 || out_rows < 0) return CAP_ERR_INVALID_ARG;
     if (!row_dtype_ok(dtype, d)) return CAP_ERR_INVALID_ARG;
     if (!aligned16(in) || !aligned16(out) || (shared_out && !aligned16(shared_out))) return CAP_ERR_INVALID_ARG;
-    if (mode == CAP_COMBINE_DEST_REDUCE) {
+    if (mode == CAP_COMBINE_DEST_REDUCE || mode == CAP_COMBINE_DEST_REDUCE_MULTI) {
         if (!w) return CAP_ERR_INVALID_ARG;
     } else if (mode == CAP_COMBINE_SRC_REDUCE) {
         if (out_rows < topo->tokens_per_rank) return CAP_ERR_INVALID_ARG;

@@ -294,6 +294,33 @@ __device__ __forceinline__ void k_loop(int KT, const uint8_t* lds, int wm, int w
     }
 }
 
+// Destination combine folded into the down GEMM's epilogue (Sec. II-C local
+// aggregation, Eq. 1): row i of the call whose token has no other kept expert
+// on the rank goes to row dst[i] of the receive-side buffer, scaled by its
+// gate weight, instead of to Y.  The storer waves load the plan of a down
+// tile's rows during its K loop into an LDS table (dst, w per row of the tile).
+struct CombinePlan {
+    const int32_t* dst;      // [max_rows] receive row, or -1: write Y (nullptr: no combine)
+    const float* w;          // [max_rows] gate weight w'
+    uint16_t* parts;         // [parts_rows][d] receive-side rows
+    int parts_rows;
+};
+
+// One 16-byte chunk (8 bf16 of a Y row) scaled by w the way the destination
+// reduce does it for a single term: fp32 fmaf(w, y, 0), then bf16 rounded to
+// nearest even (the hardware conversion gives the reduce's bits for finite
+// values).
+__device__ __forceinline__ u32x4 scale_chunk(const u32x4& v, float w) {
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const float lo = __builtin_fmaf(w, __uint_as_float(v[i] << 16), 0.0f);
+        const float hi = __builtin_fmaf(w, __uint_as_float(v[i] & 0xFFFF0000u), 0.0f);
+        o[i] = pack_bf16x2_rne(lo, hi);
+    }
+    return o;
+}
+
 // Epilogue of a tile of rows [row0, row0 + rows) and block column nt.
 // Lane (r, h) = (lane % 32, lane / 32) holds, for register group g, columns
 // 8g + 4h + 0..3 of row r of each 32 x 32 block.  Lanes r and r + 32 swap
@@ -305,9 +332,15 @@ __device__ __forceinline__ void k_loop(int KT, const uint8_t* lds, int wm, int w
 // bf16 once.  Loader waves write their 16-byte pieces to the staging area
 // (stage buffer 1), storer waves to the output; after a barrier the storers
 // also write the staged rows.  Storers never wait for their stores here.
+// Down GEMM with a combine plan (plan_dst != nullptr): a row whose plan entry
+// names a receive row in [0, parts_rows) is scaled (by the wave that holds
+// its accumulators, before staging) and written there, every other row to
+// the output.
 template <bool GUP>
 __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16_t* __restrict__ out, int N_out,
-                                           int row0, int rows, int nt, int wave, int lane, uint8_t* staging) {
+                                           int row0, int rows, int nt, int wave, int lane, uint8_t* staging,
+                                           const int* plan_dst = nullptr, const float* plan_w = nullptr,
+                                           uint16_t* __restrict__ parts = nullptr, int parts_rows = 0) {
     constexpr int OUT_C = GUP ? kWN / 2 : kWN;        // output columns of a wave tile
     constexpr int OUT_RB = OUT_C * 2;                 // bytes per staged output row
     constexpr int OUT_CH = OUT_RB / 16;               // 16-byte chunks per staged row
@@ -334,6 +367,14 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
         const int r = i * 32 + ep_row;                                 // row within the wave tile
         const bool row_ok = wm * kWM + r < rows;
         uint16_t* crow = out + static_cast<size_t>(row0 + wm * kWM + r) * N_out + out_c0;
+        int dst = -1;
+        float dw = 0.0f;
+        if (!GUP && plan_dst && row_ok) {
+            dst = plan_dst[wm * kWM + r];
+            dw = plan_w[wm * kWM + r];
+            if (static_cast<unsigned>(dst) >= static_cast<unsigned>(parts_rows)) dst = -1;
+            else if (!loader) crow = parts + static_cast<size_t>(dst) * N_out + out_c0;
+        }
 #pragma unroll
         for (int jb = 0; jb < NB; ++jb) {
             float v[16];
@@ -355,6 +396,7 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
                 u32x4 o;
                 o[0] = ra[0]; o[1] = rb[0]; o[2] = ra[1]; o[3] = rb[1];
                 const int c = jb * 4 + gp + ep_half;                   // 8-column chunk in the wave tile
+                if (dst >= 0) o = scale_chunk(o, dw);
                 if (loader) {
                     *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = o;
                 } else if (row_ok) {
@@ -378,8 +420,15 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
             const int r = r0 + ep_lane / OUT_CH;
             const int c = ep_lane % OUT_CH;
             const u32x4 vv = *reinterpret_cast<const u32x4*>(stg + r * OUT_RB + 16 * (c ^ stg_swz(r)));
-            if (lwm * kWM + r < rows)
-                *reinterpret_cast<u32x4*>(out + static_cast<size_t>(row0 + lwm * kWM + r) * N_out + l_c0 + 8 * c) = vv;
+            if (lwm * kWM + r < rows) {
+                uint16_t* orow = out + static_cast<size_t>(row0 + lwm * kWM + r) * N_out;
+                if (!GUP && plan_dst) {   // the loader wave scaled the row when it staged it
+                    const int dst = plan_dst[lwm * kWM + r];
+                    if (static_cast<unsigned>(dst) < static_cast<unsigned>(parts_rows))
+                        orow = parts + static_cast<size_t>(dst) * N_out;
+                }
+                *reinterpret_cast<u32x4*>(orow + l_c0 + 8 * c) = vv;
+            }
         }
     }
 }
@@ -488,8 +537,10 @@ template <bool GATEUP, bool GATHER>
 __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ B0, const uint16_t* __restrict__ B1,
     uint16_t* __restrict__ C, const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int K,
-    int N_out, const int32_t* __restrict__ row_src, int x_rows) {
+    int N_out, const int32_t* __restrict__ row_src, int x_rows, CombinePlan cp) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
+    __shared__ int plan_dst[kBM];
+    __shared__ float plan_w[kBM];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
     __shared__ int row_begin[kMaxExpertsLocal];
     __shared__ int row_end[kMaxExpertsLocal];
@@ -504,6 +555,29 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
     const int wm = wave / kWavesN, wn = wave % kWavesN;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
     const LaneMap lm = lane_map(lane);
+    // combine plan of a down tile: each storer lane loads one row's entry at
+    // the third stage (after the second, where the fused kernel's storers
+    // wait for their previous stores to drain) and writes it to the LDS table
+    // at the last; the epilogue reads the table after the K loop's final
+    // barrier
+    const bool comb = !GATEUP && cp.dst != nullptr;
+    int pl_d = -1;
+    float pl_w = 0.0f;
+    auto load_plan = [&](int kt, int KTn, int r0, int nrows) {
+        const int q = (wave - kNL) * kWave + lane;
+        if (kt == min(2, KTn - 1)) {
+            pl_d = -1;
+            pl_w = 0.0f;
+            if (q < nrows) {
+                pl_d = cp.dst[r0 + q];
+                pl_w = cp.w[r0 + q];
+            }
+        }
+        if (kt == KTn - 1) {
+            plan_dst[q] = pl_d;
+            plan_w[q] = pl_w;
+        }
+    };
 
     int row0 = 0, rows = 0, nt = 0;
     TileSrc src;
@@ -538,6 +612,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
             if (loader) wait_loads();              // this wave's part of stage kt has landed
             block_barrier();                       // stage kt visible; the other buffer is free
             if (loader && kt + 1 < KT) issue_stage(src, kt + 1, wave, lm, lane_off, GATHER, a_off, lds_base);
+            if (comb && !loader) load_plan(kt, KT, row0, rows);
         });
 
         // every wave is done with this tile's LDS: loaders start the next
@@ -546,7 +621,8 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
         const int cur_row0 = row0, cur_rows = rows, cur_nt = nt;
         const int next = tile + gridDim.x;
         if (next < total) start_tile(next);
-        store_tile<GATEUP>(acc, C, N_out, cur_row0, cur_rows, cur_nt, wave, lane, lds + kStageBytes);
+        store_tile<GATEUP>(acc, C, N_out, cur_row0, cur_rows, cur_nt, wave, lane, lds + kStageBytes,
+                           comb ? plan_dst : nullptr, plan_w, cp.parts, cp.parts_rows);
         tile = next;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
@@ -610,8 +686,10 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
     const uint16_t* __restrict__ W2, uint16_t* __restrict__ H, uint16_t* __restrict__ Y,
     const int32_t* __restrict__ row_offsets, int E_loc, int max_rows, int d, int inter,
     const int32_t* __restrict__ row_src, int x_rows, int n_xcc, int* __restrict__ sync,
-    int* __restrict__ wait_err, int spin_limit, int target_bias) {
+    int* __restrict__ wait_err, int spin_limit, int target_bias, CombinePlan cp) {
     __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
+    __shared__ int plan_dst[kBM];
+    __shared__ float plan_w[kBM];
     __shared__ int mt_prefix[kMaxExpertsLocal + 1];
     __shared__ int row_begin[kMaxExpertsLocal];
     __shared__ int row_end[kMaxExpertsLocal];
@@ -630,6 +708,25 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
     const int wm = wave / kWavesN, wn = wave % kWavesN;
     const uint32_t lds_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_void*)lds));
     const LaneMap lm = lane_map(lane);
+    // combine plan of a down tile (as in the two-kernel path)
+    const bool comb = cp.dst != nullptr;
+    int pl_d = -1;
+    float pl_w = 0.0f;
+    auto load_plan = [&](int kt, int KTn, int r0, int nrows) {
+        const int q = (wave - kNL) * kWave + lane;
+        if (kt == min(2, KTn - 1)) {
+            pl_d = -1;
+            pl_w = 0.0f;
+            if (q < nrows) {
+                pl_d = cp.dst[r0 + q];
+                pl_w = cp.w[r0 + q];
+            }
+        }
+        if (kt == KTn - 1) {
+            plan_dst[q] = pl_d;
+            plan_w[q] = pl_w;
+        }
+    };
 
     // queue of XCD slot x: m-tiles [mb, mb + MX); gate/up entries [0, GU), down [GU, Q)
     int x = xcc_register() % n_xcc;
@@ -740,6 +837,7 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
                 if (loader) wait_loads();
                 block_barrier();
                 if (kt + 1 < KT) issue(kt + 1);
+                if (comb && !T.gu && !loader) load_plan(kt, KT, T.row0, T.rows);
                 if (ahead) {
                     if (kt == 0 && wave == kNL && lane == 0) claim = atomic_add_agent(queue, 1);
                     if (kt == 1) {
@@ -782,7 +880,8 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
                 if (early) issue(0);
             }
             if (C.gu) store_tile<true>(acc, H, inter, C.row0, C.rows, C.nt, wave, lane, lds + kStageBytes);
-            else store_tile<false>(acc, Y, d, C.row0, C.rows, C.nt, wave, lane, lds + kStageBytes);
+            else store_tile<false>(acc, Y, d, C.row0, C.rows, C.nt, wave, lane, lds + kStageBytes,
+                                   comb ? plan_dst : nullptr, plan_w, cp.parts, cp.parts_rows);
             if (C.gu) pending = C.m;
             if (nx < Q && !early) {
                 deliver();                         // the next tile may need this tile's rows
@@ -930,10 +1029,15 @@ cap_status ffn_supported(cap_dtype dt, int d, int inter) {
 }
 
 // row_src == nullptr: xs holds the expert-sorted rows; otherwise row i is
-// xs[row_src[i]] and xs has x_rows rows.
+// xs[row_src[i]] and xs has x_rows rows.  row_dst != nullptr (bf16 only): the
+// destination combine of single-expert tokens goes into the down GEMM's
+// epilogue (row_dst, row_w, parts, parts_rows: CombinePlan).
 cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_rows, const void* xs, int x_rows,
                              const int32_t* row_src, const int32_t* row_offsets, const void* w1, const void* w3,
-                             const void* w2, void* y, void* ws, const cap_ffn_options* opt, hipStream_t st) {
+                             const void* w2, void* y, void* ws, const cap_ffn_options* opt, hipStream_t st,
+                             const int32_t* row_dst, const float* row_w, void* parts, int parts_rows) {
+    const CombinePlan cp{row_dst, row_w, static_cast<uint16_t*>(parts), parts_rows};
+    const CombinePlan none{nullptr, nullptr, nullptr, 0};
     if (dt == CAP_DTYPE_BF16) {
         const auto* a = static_cast<const uint16_t*>(xs);
         const auto* b1 = static_cast<const uint16_t*>(w1);
@@ -959,11 +1063,11 @@ cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_
             if (row_src)
                 ffn_fused_bf16_kernel<true><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
                                                                        max_rows, d, inter, row_src, x_rows, n_xcc, sync,
-                                                                       err, spin, bias);
+                                                                       err, spin, bias, cp);
             else
                 ffn_fused_bf16_kernel<false><<<g, kNW * kWave, 0, st>>>(a, b1, b3, b2, h, out, row_offsets, E_loc,
                                                                         max_rows, d, inter, nullptr, 0, n_xcc, sync,
-                                                                        err, spin, bias);
+                                                                        err, spin, bias, cp);
             CAP_LAUNCH_CHECK();
             return CAP_OK;
         }
@@ -971,14 +1075,14 @@ cap_status expert_ffn_launch(cap_dtype dt, int E_loc, int d, int inter, int max_
         const int g1 = persistent_grid(mt_upper * (inter / (kBN / 2)));
         if (row_src)
             ffn_gemm_bf16_kernel<true, true><<<g1, kNW * kWave, 0, st>>>(a, b1, b3, h, row_offsets, E_loc, max_rows, d,
-                                                                         inter, row_src, x_rows);
+                                                                         inter, row_src, x_rows, none);
         else
             ffn_gemm_bf16_kernel<true, false><<<g1, kNW * kWave, 0, st>>>(a, b1, b3, h, row_offsets, E_loc, max_rows, d,
-                                                                          inter, nullptr, 0);
+                                                                          inter, nullptr, 0, none);
         CAP_LAUNCH_CHECK();
         const int g2 = persistent_grid(mt_upper * (d / kBN));
         ffn_gemm_bf16_kernel<false, false><<<g2, kNW * kWave, 0, st>>>(h, b2, nullptr, out, row_offsets, E_loc,
-                                                                       max_rows, inter, d, nullptr, 0);
+                                                                       max_rows, inter, d, nullptr, 0, cp);
         CAP_LAUNCH_CHECK();
     } else {
         const long long mt_upper = (static_cast<long long>(max_rows) + kF32Tile - 1) / kF32Tile + E_loc;

@@ -180,6 +180,42 @@ __global__ __launch_bounds__(kThreads) void row_source_kernel(
     }
 }
 
+// Row plan for the FFN with the destination combine folded in: the row
+// source, and for a row whose token has no other kept slot on the rank (one
+// term in its destination reduce), the receive row the term goes to and its
+// gate weight; -1 and 0 otherwise (also when the receive row is at or past
+// parts_rows).  The count of a token's rows on the rank is the destination
+// reduce's own (kept slots whose expert-sorted row lies in the rank's range).
+__global__ __launch_bounds__(kThreads) void row_plan_kernel(
+    Topo g, int rank, const float* __restrict__ w, const int32_t* __restrict__ slot_pos,
+    const int32_t* __restrict__ expert_offsets, const int32_t* __restrict__ recv_offsets,
+    const int32_t* __restrict__ recv_token, int32_t* __restrict__ row_src, int32_t* __restrict__ row_dst,
+    float* __restrict__ row_w, int rows_cap, int parts_rows) {
+    const int r0 = recv_offsets[rank];
+    if (r0 < 0) return;
+    const int U = min(recv_offsets[rank + 1] - r0, g.T * g.k - r0);
+    const int base = expert_offsets[rank * g.E_loc];
+    const int rows_r = min(expert_offsets[(rank + 1) * g.E_loc] - base, rows_cap);
+    const long long items = static_cast<long long>(U) * g.k;
+    for (long long i = static_cast<long long>(blockIdx.x) * kThreads + threadIdx.x; i < items;
+         i += static_cast<long long>(gridDim.x) * kThreads) {
+        const int u = static_cast<int>(i / g.k);
+        const int s = static_cast<int>(i - static_cast<long long>(u) * g.k);
+        const int t = recv_token[r0 + u];
+        if (static_cast<unsigned>(t) >= static_cast<unsigned>(g.T)) continue;
+        const size_t q0 = static_cast<size_t>(t) * g.k;
+        const int rr = slot_pos[q0 + s] - base;
+        if (static_cast<unsigned>(rr) >= static_cast<unsigned>(rows_r)) continue;
+        int n = 0;
+        for (int s2 = 0; s2 < g.k; ++s2)
+            n += static_cast<unsigned>(slot_pos[q0 + s2] - base) < static_cast<unsigned>(rows_r) ? 1 : 0;
+        const bool single = n == 1 && r0 + u < parts_rows;
+        row_src[rr] = t;
+        row_dst[rr] = single ? r0 + u : -1;
+        row_w[rr] = single ? w[q0 + s] : 0.0f;
+    }
+}
+
 // ---------------------------------------------------------------- send pack
 template <int JB>
 __global__ __launch_bounds__(kThreads) void send_pack_kernel(
@@ -237,7 +273,7 @@ __global__ __launch_bounds__(kThreads) void dest_reduce_kernel(
     Topo g, int rank, int vpr, int pieces, const u32x4* __restrict__ Y, const float* __restrict__ w,
     const int32_t* __restrict__ slot_pos, const int32_t* __restrict__ expert_offsets,
     const int32_t* __restrict__ recv_offsets, const int32_t* __restrict__ recv_token,
-    u32x4* __restrict__ out, int in_rows, int out_rows) {
+    u32x4* __restrict__ out, int in_rows, int out_rows, int skip_single) {
     const int r0 = recv_offsets[rank];
     if (r0 < 0) return;
     const int U = min(min(recv_offsets[rank + 1] - r0, g.T * g.k - r0), out_rows - r0);
@@ -262,6 +298,7 @@ __global__ __launch_bounds__(kThreads) void dest_reduce_kernel(
         // slot-ordered list of (row, weight)
         uint64_t vb = __ballot(row >= 0);
         const int n = __popcll(vb);
+        if (skip_single && n == 1) continue;       // written by the FFN's epilogue (wave-uniform)
         int rows[kMaxK];
         float wt[kMaxK];
 #pragma unroll
@@ -435,6 +472,20 @@ int row_grid(long long items_upper) {
 
 }  // namespace
 
+cap_status row_plan_launch(const cap_topology* tp, int rank, const float* w, const cap_layout* lay, int32_t* row_src,
+                           int32_t* row_dst, float* row_w, int rows_cap, int parts_rows, hipStream_t st) {
+    const Topo g = make_topo(tp);
+    const long long items = static_cast<long long>(g.T) * g.k;
+    long long grid = (items + kThreads - 1) / kThreads;
+    const long long cap = static_cast<long long>(device_cu_count()) * 8;
+    grid = grid < 1 ? 1 : (grid < cap ? grid : cap);
+    row_plan_kernel<<<static_cast<int>(grid), kThreads, 0, st>>>(g, rank, w, lay->slot_pos, lay->expert_offsets,
+                                                                 lay->recv_offsets, lay->recv_token, row_src,
+                                                                 row_dst, row_w, rows_cap, parts_rows);
+    CAP_LAUNCH_CHECK();
+    return CAP_OK;
+}
+
 cap_status permute_launch(const cap_topology* tp, cap_permute_mode mode, int rank, cap_dtype dt, int d,
                           const void* x, const int32_t* idx, const uint8_t* keep, const uint64_t* mask,
                           const cap_layout* lay, void* out, int out_rows, hipStream_t st) {
@@ -478,17 +529,18 @@ cap_status combine_launch(const cap_topology* tp, cap_combine_mode mode, int ran
     const u32x4* iv = static_cast<const u32x4*>(in);
     const u32x4* sv = static_cast<const u32x4*>(shared_out);
     u32x4* ov = static_cast<u32x4*>(out);
-    if (mode == CAP_COMBINE_DEST_REDUCE) {
+    if (mode == CAP_COMBINE_DEST_REDUCE || mode == CAP_COMBINE_DEST_REDUCE_MULTI) {
+        const int skip = mode == CAP_COMBINE_DEST_REDUCE_MULTI ? 1 : 0;
         const int pieces = row_pieces(g.T, vpr);
         const int grid = row_grid(static_cast<long long>(g.T) * pieces);
         if (dt == CAP_DTYPE_BF16)
             dest_reduce_kernel<Bf16Row, 2><<<grid, kThreads, 0, st>>>(
                 g, rank, vpr, pieces, iv, w, lay->slot_pos, lay->expert_offsets, lay->recv_offsets,
-                lay->recv_token, ov, in_rows, out_rows);
+                lay->recv_token, ov, in_rows, out_rows, skip);
         else
             dest_reduce_kernel<F32Row, 2><<<grid, kThreads, 0, st>>>(
                 g, rank, vpr, pieces, iv, w, lay->slot_pos, lay->expert_offsets, lay->recv_offsets,
-                lay->recv_token, ov, in_rows, out_rows);
+                lay->recv_token, ov, in_rows, out_rows, skip);
     } else {
         const int pieces = row_pieces(g.tpr, vpr);
         const int grid = row_grid(static_cast<long long>(g.tpr) * pieces);

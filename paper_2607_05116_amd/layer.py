@@ -77,6 +77,8 @@ class DeviceLayer:
         self.recv_cap = recv_cap if recv_cap is not None else T * min(k, R)
         self.xs = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
         self.row_src = torch.empty(self.row_cap, **i32)
+        self.row_dst = torch.empty(self.row_cap, **i32)
+        self.row_w = torch.empty(self.row_cap, dtype=torch.float32, device=self.dev)
         self.Y = torch.empty((self.row_cap, d), dtype=self.tdt, device=self.dev)
         self.parts = torch.zeros((self.recv_cap, d), dtype=self.tdt, device=self.dev)
         self.y = torch.empty((cfg.tokens_per_rank, d), dtype=self.tdt, device=self.dev)
@@ -88,6 +90,8 @@ class DeviceLayer:
         self.weights: dict[int, tuple] = {}
         self.naive = False              # expert-level threshold pruning instead of CAP's
         self.fused_gather = True        # FFN reads x through row_src instead of a gathered copy
+        # bf16: single-expert tokens' destination combine in the FFN's epilogue
+        self.fused_combine = cfg.dtype == "bf16"
         self.shared = None
         self.shared_out = None
         self.ws_shared = None
@@ -148,6 +152,12 @@ class DeviceLayer:
         capi.cap_permute(self.topo, capi.CAP_PERMUTE_ROW_SOURCE, rank, self.dt, self.d, None,
                          self.idx, self.keep, self.mask, self.lay, self.row_src, self.row_cap, stream)
 
+    def row_plan(self, rank: int, stream=None):
+        """Row source plus the receive row and gate weight of each row whose
+        token has no other kept expert on the rank."""
+        capi.cap_row_plan(self.topo, rank, self.w, self.lay, self.row_src, self.row_dst, self.row_w,
+                          self.row_cap, self.recv_cap, stream)
+
     def send_pack(self, rank: int, out: torch.Tensor, stream=None):
         capi.cap_permute(self.topo, capi.CAP_PERMUTE_SEND_PACK, rank, self.dt, self.d, self.x,
                          self.idx, self.keep, self.mask, self.lay, out, out.shape[0], stream)
@@ -168,6 +178,17 @@ class DeviceLayer:
                                self.x.shape[0], self.row_src, offs, w1, w3, w2, self.Y, self.ws_ffn,
                                options=self.ffn_opts, stream=stream)
 
+    def ffn_combine(self, rank: int, stream=None):
+        """ffn_gather with the single-expert tokens' destination combine in the
+        down GEMM's epilogue (their rows go to parts, scaled; the rest to Y)."""
+        w1, w3, w2 = self.weights[rank]
+        E_loc = self.cfg.E_loc
+        offs = self.lay_t["expert_offsets"][rank * E_loc:(rank + 1) * E_loc + 1]
+        capi.cap_expert_ffn_combine(self.dt, E_loc, self.d, self.cfg.inter, self.row_cap, self.x,
+                                    self.x.shape[0], self.row_src, offs, w1, w3, w2, self.Y, self.row_dst,
+                                    self.row_w, self.parts, self.recv_cap, self.ws_ffn, options=self.ffn_opts,
+                                    stream=stream)
+
     def shared_ffn(self, rank: int, stream=None):
         if self.shared is None:
             return
@@ -179,6 +200,13 @@ class DeviceLayer:
 
     def dest_reduce(self, rank: int, stream=None):
         capi.cap_combine(self.topo, capi.CAP_COMBINE_DEST_REDUCE, rank, self.dt, self.d, self.Y,
+                         self.row_cap, self.idx, self.w, self.keep, self.mask, self.lay, None,
+                         self.parts, self.recv_cap, stream)
+
+    def dest_reduce_multi(self, rank: int, stream=None):
+        """The destination reduce of the tokens with two or more kept experts
+        on the rank (after ffn_combine)."""
+        capi.cap_combine(self.topo, capi.CAP_COMBINE_DEST_REDUCE_MULTI, rank, self.dt, self.d, self.Y,
                          self.row_cap, self.idx, self.w, self.keep, self.mask, self.lay, None,
                          self.parts, self.recv_cap, stream)
 
@@ -220,19 +248,27 @@ class DeviceLayer:
         the source reduce waits for, when the shared experts ran on another
         stream; without it they run here, before the source reduce."""
         main = stream if stream is not None else torch.cuda.current_stream()
-        if self.fused_gather:
+        combine = self.fused_gather and self.fused_combine
+        if combine:
+            self.row_plan(rank, main)
+        elif self.fused_gather:
             self.row_source(rank, main)
         else:
             self.gather(rank, main)
         if ffn_events is not None:
             ffn_events[0].record(main)
-        if self.fused_gather:
+        if combine:
+            self.ffn_combine(rank, main)
+        elif self.fused_gather:
             self.ffn_gather(rank, main)
         else:
             self.ffn(rank, main)
         if ffn_events is not None:
             ffn_events[1].record(main)
-        self.dest_reduce(rank, main)
+        if combine:
+            self.dest_reduce_multi(rank, main)
+        else:
+            self.dest_reduce(rank, main)
         if join is None:
             self.shared_ffn(rank, main)
         else:

@@ -159,6 +159,32 @@ def test_permute_and_combine_validation(capi):
     assert small_out == capi.CAP_ERR_INVALID_ARG
 
 
+def test_row_plan_and_ffn_combine_validation(capi):
+    """The folded destination combine's calls reject bad arguments before
+    launching anything."""
+    t = _topo(capi)
+    lay = capi.Layout(*([0x10000] * 10))
+    plan = capi._lib.cap_row_plan
+    by = ctypes.byref
+    assert plan(by(t), 0, None, by(lay), 0x2000, 0x3000, 0x4000, 100, 100, None) == capi.CAP_ERR_INVALID_ARG
+    assert plan(by(t), 4, 0x1000, by(lay), 0x2000, 0x3000, 0x4000, 100, 100, None) == capi.CAP_ERR_INVALID_ARG
+    assert plan(by(t), 0, 0x1000, by(lay), 0x2000, 0x3001, 0x4000, 100, 100, None) == capi.CAP_ERR_INVALID_ARG
+    assert plan(by(t), 0, 0x1000, by(lay), 0x2000, 0x3000, 0x4000, -1, 100, None) == capi.CAP_ERR_INVALID_ARG
+    assert plan(by(t), 0, 0x1000, by(lay), 0x2000, 0x3000, None, 100, 100, None) == capi.CAP_ERR_INVALID_ARG
+    f = capi._lib.cap_expert_ffn_combine
+    B, F = capi.CAP_DTYPE_BF16, capi.CAP_DTYPE_F32
+    head = (0x10000, 512, 0x20000, 0x30000, 0x40000, 0x50000, 0x60000, 0x70000)
+    ws = (0x80000, 1 << 30, None, None)
+    assert f(F, 4, 128, 256, 100, *head, 0x90000, 0xA0000, 0xB0000, 100, *ws) == capi.CAP_ERR_UNSUPPORTED
+    assert f(B, 4, 2048, 768, 100, *head, None, 0xA0000, 0xB0000, 100, *ws) == capi.CAP_ERR_INVALID_ARG
+    assert f(B, 4, 2048, 768, 100, *head, 0x90000, 0xA0000, 0xB0008, 100, *ws) == capi.CAP_ERR_INVALID_ARG
+    assert f(B, 4, 2048, 768, 100, *head, 0x90000, 0xA0000, 0xB0000, -1, *ws) == capi.CAP_ERR_INVALID_ARG
+    assert f(B, 4, 2000, 768, 100, *head, 0x90000, 0xA0000, 0xB0000, 100, *ws) == capi.CAP_ERR_UNSUPPORTED
+    multi_no_w = capi._lib.cap_combine(by(t), capi.CAP_COMBINE_DEST_REDUCE_MULTI, 0, 1, 128, 0x1000, 10, 0x2000,
+                                       None, 0x4000, 0x5000, by(lay), None, 0x6000, 63, None)
+    assert multi_no_w == capi.CAP_ERR_INVALID_ARG
+
+
 def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
