@@ -148,3 +148,30 @@ def test_ffn_combine_equals_separate_path(name, kind, p, ranks, own_cap):
             print(f"[{name} rank {rank} parts_rows {parts_rows}] rows {n}, rows through Y {len(multi)}", flush=True)
         assert L.ffn_wait_errors() == 0
         del L.weights[rank]
+
+
+def test_idle_rank_combine_calls_are_empty():
+    """A rank whose experts are never selected: its row plan, combining FFN
+    and multi-term destination reduce write nothing."""
+    name, p = "c2", 0.3
+    cfg = gen.CONFIGS[name]
+    er, el = gen.sequential_placement(cfg)
+    logits = C.logits(name).copy()
+    idle = cfg.R - 1
+    logits[:, er == idle] -= 60.0                     # never in any token's top k
+    L = DeviceLayer(cfg, logits, gen.activations(cfg), er, el, p, 5.0)
+    L.set_rank_weights(idle, *C.rank_weights(cfg, er, el, idle))
+    L.front()
+    torch.cuda.synchronize()
+    assert L.rank_rows(idle) == 0
+    L.parts.view(torch.int16).fill_(0x1234)
+    L.Y.view(torch.int16).fill_(0x1234)
+    L.row_dst.fill_(-5)
+    L.row_plan(idle)
+    L.ffn_combine(idle)
+    L.dest_reduce_multi(idle)
+    torch.cuda.synchronize()
+    assert bool((L.parts.view(torch.int16) == 0x1234).all())
+    assert bool((L.Y.view(torch.int16) == 0x1234).all())
+    assert bool((L.row_dst == -5).all())
+    assert L.ffn_wait_errors() == 0

@@ -180,10 +180,13 @@ def test_step_with_side_stream_matches_serial(name):
         L.set_shared_weights(*gen.shared_weights(cfg))
     g0 = torch.Generator(device="cuda").manual_seed(3)
     L.parts.copy_((torch.randn(L.parts.shape, generator=g0, device="cuda") * 0.05).to(L.tdt))
+    # Y holds only the rows the FFN does not combine into parts itself: start
+    # every run from the same contents
+    L.Y.zero_()
     L.step(0)
     torch.cuda.synchronize()
     rows = L.rank_rows(0)
-    names = ("y", "Y", "coact", "shared_out") if cfg.n_shared else ("y", "Y", "coact")
+    names = ("y", "Y", "parts", "coact") + (("shared_out",) if cfg.n_shared else ())
 
     def snap(n):
         v = L.host(n)
@@ -272,15 +275,16 @@ def test_graph_replay_matches_eager():
     g0 = torch.Generator(device="cuda").manual_seed(11)
     L.parts.copy_((torch.randn(L.parts.shape, generator=g0, device="cuda") * 0.05).to(L.tdt))
     side = torch.cuda.Stream()
+    L.Y.zero_()                                    # rows combined into parts by the FFN stay as they are
     L.front(side=side)
     L.rank_path(0)
     torch.cuda.synchronize()
-    names = ("y", "Y", "coact", "idx", "w", "mask", "row_src")
-    rows = L.rank_rows(0)                          # Y and row_src past this are capacity, never written
+    names = ("y", "Y", "parts", "coact", "idx", "w", "mask", "row_src", "row_dst", "row_w")
+    rows = L.rank_rows(0)                          # Y and the row plan past this are capacity, never written
 
     def snap(n):
         v = L.host(n)
-        return v[:rows].copy() if n in ("Y", "row_src") else v.copy()
+        return v[:rows].copy() if n in ("Y", "row_src", "row_dst", "row_w") else v.copy()
 
     want = {n: snap(n) for n in names}
     graph = L.capture_step(0, side=side)
