@@ -8,7 +8,10 @@
  *   communication-aware device-level pruning (Sec. VI, Eq. 6 and its greedy);
  *   the device-centric all-to-all layout and send volume (Sec. II-C, Eq. 3);
  *   token permutation; SwiGLU expert FFN over one rank's experts; the weighted
- *   combine (Sec. II-C, Eq. 1); expert co-activation counts (Sec. IV-B).
+ *   combine (Sec. II-C, Eq. 1), also folded into the FFN for tokens with one
+ *   kept expert on the rank; expert co-activation counts (Sec. IV-B); the
+ *   expert-level pruning baseline (Sec. II-D); the Adjustment Approach's
+ *   placement spectrum (Sec. V).
  * Expert-parallel ranks are virtual: all of them live on the one GPU.
  *
  * Conventions for every call

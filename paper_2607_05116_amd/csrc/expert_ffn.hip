@@ -16,10 +16,15 @@
 //   * Half of the waves issue all the stage loads and the other half all the
 //     output stores, so no wave's in-order memory counter mixes the two (a
 //     wait for a stage never waits for a tile's worth of stores to drain).
+//   * Each wave reads its LDS fragments one MFMA K step ahead of its MFMAs.
 //   * Calls of many m-tiles run both GEMMs in one persistent kernel with a
 //     tile queue per XCD (ffn_fused_bf16_kernel); calls of few m-tiles run one
 //     persistent kernel per GEMM (ffn_gemm_bf16_kernel).  Every output element
 //     takes the same arithmetic in both, so the two give identical bits.
+//   * Optionally (a combine plan) the down GEMM's epilogue writes the rows of
+//     tokens with a single kept expert on the rank, scaled by their gate
+//     weight, into the receive-side buffer instead of Y (Sec. II-C local
+//     aggregation of a one-term sum).
 // fp32 path: a plain LDS-tiled FMA kernel (small shapes only).
 #include "cap_device.hpp"
 

@@ -1,6 +1,8 @@
 // Token permutation and weighted combine (Sec. II-C; Eq. 1).
 //
-// All four kernels are HBM-bound row movers built the same way:
+// The index kernels (row source, row plan) write one int per expert-sorted
+// row from one thread per (received token, slot).  The four row movers are
+// HBM-bound and built the same way:
 //   * one wave owns one row piece at a time (a token's row, or a contiguous
 //     part of it when there are too few tokens to fill the chip);
 //   * the token's k routing slots are read one slot per lane, so a token's
@@ -16,7 +18,9 @@
 //   send pack      (source rank s) read each token of s once, write one row per
 //                  kept destination device into the send buffer.
 //   dest reduce    (rank r) per received token: sum of w'_s * Y over the token's
-//                  kept experts on r (local aggregation before the return).
+//                  kept experts on r (local aggregation before the return); a
+//                  mode skips the tokens with one row on r, whose one-term
+//                  sum the FFN's epilogue writes (row plan).
 //   src reduce     (rank s) per token of s: sum of the rows every kept device
 //                  returned (+ the shared experts' output).
 // Accumulation is fp32 in a fixed order (slot order / ascending device).
