@@ -92,6 +92,9 @@ class DeviceLayer:
         self.fused_gather = True        # FFN reads x through row_src instead of a gathered copy
         # bf16: single-expert tokens' destination combine in the FFN's epilogue
         self.fused_combine = cfg.dtype == "bf16"
+        # with a side stream: start the shared experts after the routing front
+        # end (True) or with it (False)
+        self.shared_after_front = False
         self.shared = None
         self.shared_out = None
         self.ws_shared = None
@@ -305,11 +308,14 @@ class DeviceLayer:
                 if not hasattr(self, "_step_ev"):
                     self._step_ev = [torch.cuda.Event() for _ in range(3)]
                 start, _, side_done = self._step_ev
+                if self.shared_after_front:
+                    self.front(main)
                 start.record(main)
                 side.wait_event(start)
                 self.shared_ffn(rank, side)
                 side_done.record(side)
-                self.front(main)
+                if not self.shared_after_front:
+                    self.front(main)
                 self.rank_path(rank, main, ffn_events, join=side_done)
                 return
             self.front(main)
