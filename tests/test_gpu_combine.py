@@ -175,3 +175,68 @@ def test_idle_rank_combine_calls_are_empty():
     assert bool((L.Y.view(torch.int16) == 0x1234).all())
     assert bool((L.row_dst == -5).all())
     assert L.ffn_wait_errors() == 0
+
+
+def test_c5_step_receive_rows_against_oracle():
+    """The DeepSeek-V3-shaped step (folded combine) against the fp64 oracle on
+    sampled received tokens of rank 0: 200 whose only kept expert on the rank
+    makes the FFN's epilogue write their row, and 200 with several, which the
+    multi-term reduce sums (Eq. 1 over the kept experts on the rank, Sec. II-C)."""
+    name, kind, p = "c5", "coact", 0.1
+    cfg = gen.CONFIGS[name]
+    er, el = C.placement(name, kind, p, 5.0)
+    r, lay = C.oracle_routing(name, kind, p, 5.0)
+    x = gen.activations(cfg)
+    L = _layer(name, kind, p, x=x)
+    L.set_rank_weights(0, *C.rank_weights(cfg, er, el, 0))
+    L.set_shared_weights(*gen.shared_weights(cfg))
+    L.parts.zero_()
+    L.step(0)
+    torch.cuda.synchronize()
+    assert L.ffn_wait_errors() == 0
+    eo = lay["expert_offsets"].astype(np.int64)
+    base, rows_r = int(eo[0]), int(eo[cfg.E_loc] - eo[0])
+    U0 = int(lay["recv_offsets"][1])
+    sp = lay["slot_pos"].astype(np.int64) - base
+    toks = lay["recv_token"][:U0].astype(np.int64)
+    mine = (sp[toks] >= 0) & (sp[toks] < rows_r)              # [U0][k]
+    n = mine.sum(axis=1)
+    rng = np.random.default_rng(5)
+    single = rng.choice(np.flatnonzero(n == 1), 200, replace=False)
+    multi = rng.choice(np.flatnonzero(n >= 2), 200, replace=False)
+    us = np.concatenate([single, multi])
+    row_tok = {}
+    for u in us:
+        for s in range(cfg.k):
+            if mine[u, s]:
+                row_tok[int(sp[toks[u], s])] = int(toks[u])
+    rows = np.array(sorted(row_tok), np.int64)
+    Y = dict(zip(rows.tolist(), _oracle_rows(cfg, er, el, lay, x, rows, [row_tok[i] for i in rows.tolist()])))
+    ref = np.zeros((len(us), cfg.d), np.float64)
+    for i, u in enumerate(us):
+        t = toks[u]
+        for s in range(cfg.k):
+            if mine[u, s]:
+                ref[i] += float(r["wp"][t, s]) * Y[int(sp[t, s])]
+    got = L.parts[torch.from_numpy(us).to(L.parts.device)].float().cpu().numpy()
+    print(f"[c5 step] received {U0}, sampled {len(us)} tokens over {len(rows)} expert rows", flush=True)
+    ok, worst = C.within_tol(got, ref)
+    assert ok, worst
+    assert C.rel_fro(got, ref) <= 1e-2
+
+
+def _oracle_rows(cfg, er, el, lay, x, rows, tokens):
+    """fp64 oracle SwiGLU of the given rows of rank 0's expert-sorted buffer
+    (row i holds x of token tokens[i], the expert gather's definition)."""
+    import oracle
+    eo = lay["expert_offsets"][: cfg.E_loc + 1].astype(np.int64)
+    xs32 = gen.bf16_bits_to_f32(x[np.asarray(tokens, np.int64)])
+    ids = C.local_experts(er, el, 0, cfg.E_loc)
+    out = np.zeros((len(rows), cfg.d), np.float64)
+    for l in range(cfg.E_loc):
+        a, b = eo[l] - eo[0], eo[l + 1] - eo[0]
+        sel = np.flatnonzero((rows >= a) & (rows < b))
+        if len(sel):
+            W1, W3, W2 = gen.expert_weights_f32(cfg, ids[l])
+            out[sel] = oracle.swiglu_rows(xs32[sel], W1, W3, W2)
+    return out
