@@ -276,3 +276,39 @@ def test_queue_order_groups_m_tiles():
     first = q[:32]
     assert len({m for _, m, _ in first}) == GROUP_M
     assert len({nt for _, _, nt in first}) == 32 // GROUP_M
+
+
+def test_combine_plan_indices_in_bounds():
+    """The combine plan's indices (cap_expert_ffn_combine): every storer lane's
+    LDS table slot, every epilogue read of the table (own rows and staged
+    rows) lies in [0, BM); a receive row is used only when it lies in
+    [0, parts_rows) (the kernel's unsigned compare), and then every 16-byte
+    store of the row lies inside parts; other rows go to Y as before."""
+    lane = np.arange(64)
+    # table writes: storer waves NL..NW-1, one row per lane
+    q = np.concatenate([(w - NL) * 64 + lane for w in range(NL, NW)])
+    assert q.min() == 0 and q.max() == BM - 1 and len(set(q.tolist())) == BM
+    # own-row reads (storer waves) and staged-row reads (storer w reads loader w - NL's rows)
+    for w in range(NW):
+        wm = w // WAVES_N
+        r = np.arange(MI)[:, None] * 32 + (lane & 31)[None, :]
+        assert (wm * WM + r).min() >= 0 and (wm * WM + r).max() < BM
+    for gu, out_rb in ((0, (WN) * 2),):
+        rows_per_read = 1024 // out_rb
+        for w in range(NL, NW):
+            lw = w - NL
+            lwm = lw // WAVES_N
+            r = np.arange(0, WM, rows_per_read)[:, None] + (lane // (out_rb // 16))[None, :]
+            assert (lwm * WM + r).max() < BM
+    # receive rows: the unsigned compare keeps [0, parts_rows); stores stay in parts
+    d = 7168
+    for parts_rows in (0, 1, 1000):
+        dst = np.array([-1, 0, parts_rows - 1, parts_rows, 2 ** 31 - 1], np.int64)
+        used = (dst.astype(np.uint32) < np.uint32(parts_rows)) if parts_rows > 0 else np.zeros(len(dst), bool)
+        for nt in range(d // BN):
+            for wn in range(WAVES_N):
+                c0 = nt * BN + wn * WN
+                chunks = c0 + 8 * np.arange(WN // 8)
+                for v in dst[used]:
+                    assert 0 <= v < parts_rows
+                    assert v * d + chunks.max() + 8 <= parts_rows * d
