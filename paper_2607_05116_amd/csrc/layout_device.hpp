@@ -33,13 +33,14 @@ __device__ __forceinline__ void chunk_range(const Geom& g, int c, int& t0, int& 
     t1 = min(t0 + kChunk, (src + 1) * g.tpr);
 }
 
+// Both table entries are read before either is tested, so the two loads are
+// in flight together.
 __device__ __forceinline__ int slot_position(const int32_t* er, const int32_t* el, int e, const Geom& g) {
     if (static_cast<unsigned>(e) >= static_cast<unsigned>(g.E)) return -1;
     const int r = er[e], l = el[e];
-    if (static_cast<unsigned>(r) >= static_cast<unsigned>(g.R) ||
-        static_cast<unsigned>(l) >= static_cast<unsigned>(g.E_loc))
-        return -1;
-    return r * g.E_loc + l;
+    const bool ok = (static_cast<unsigned>(r) < static_cast<unsigned>(g.R)) &
+                    (static_cast<unsigned>(l) < static_cast<unsigned>(g.E_loc));
+    return ok ? r * g.E_loc + l : -1;
 }
 
 __device__ __forceinline__ uint64_t device_bits(uint64_t m, int R) {
@@ -202,7 +203,51 @@ __global__ __launch_bounds__(kChunk) void layout_colscan_kernel(Geom g, Workspac
 }
 
 // ---------------------------------------------------------------- 3. scatter
-// Scatter of chunk bid (one block of kChunk threads per chunk).
+// Exclusive scans of two values over the 256 threads of a block in one pass;
+// *total_a / *total_b get the sums.
+__device__ __forceinline__ void block_exclusive_scan2(int a, int b, int (*wsum)[kWavesPerChunk], int& ea, int& eb,
+                                                      int* total_a, int* total_b) {
+    const int lane = lane_id(), wave = threadIdx.x / kWave;
+    int ia = a, ib = b;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int na = __shfl_up(ia, off), nb = __shfl_up(ib, off);
+        if (lane >= off) {
+            ia += na;
+            ib += nb;
+        }
+    }
+    if (lane == kWave - 1) {
+        wsum[0][wave] = ia;
+        wsum[1][wave] = ib;
+    }
+    __syncthreads();
+    int before_a = 0, before_b = 0, all_a = 0, all_b = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerChunk; ++w) {
+        if (w < wave) {
+            before_a += wsum[0][w];
+            before_b += wsum[1][w];
+        }
+        all_a += wsum[0][w];
+        all_b += wsum[1][w];
+    }
+    __syncthreads();
+    *total_a = all_a;
+    *total_b = all_b;
+    ea = before_a + ia - a;
+    eb = before_b + ib - b;
+}
+
+// Scatter of chunk bid (one block of kChunk threads per chunk).  Every global
+// load that does not depend on another is issued first, so the block waits
+// for one round of memory latency before its LDS work: the placement tables,
+// the column totals, the chunk's column bases, the token's slots and mask, and
+// in block 0 the rank-boundary bases that give send_counts (send_offsets then
+// come from a per-rank scan in LDS).
+constexpr int kSendPerThread = kMaxR * kMaxR / kChunk;   // (s, d) pairs per thread in block 0
+static_assert(kMaxR * kMaxR % kChunk == 0, "send-count pairs split evenly over the block");
+
 __device__ __forceinline__ void layout_scatter_block(
     const Geom& g, const int32_t* __restrict__ idx, const uint8_t* __restrict__ keep,
     const uint64_t* __restrict__ mask, const int32_t* __restrict__ er, const int32_t* __restrict__ el,
@@ -215,62 +260,113 @@ __device__ __forceinline__ void layout_scatter_block(
     __shared__ int pos_lds[kMaxE];
     __shared__ int32_t gbase[kMaxW];
     __shared__ int32_t roff[kMaxR + 1];
-    __shared__ int wsum[kWavesPerChunk];
-    const int wave = threadIdx.x / kWave;
-    for (int i = threadIdx.x; i < kWavesPerChunk * g.W; i += blockDim.x) bits[i / g.W][i % g.W] = 0ull;
-    for (int e = threadIdx.x; e < g.E; e += blockDim.x) pos_lds[e] = slot_position(er, el, e, g);
+    __shared__ int wsum[2][kWavesPerChunk];
+    __shared__ int32_t sc_lds[kMaxR * kMaxR];
+    const int i = threadIdx.x;                  // E <= 256 = blockDim.x
+    const int wave = i / kWave;
 
-    // expert offsets (slot-position order) and receive offsets from the column totals
+    // ---- one round of independent loads
     const int32_t* cb = ws.part + static_cast<size_t>(bid) * g.sub * g.W;     // the chunk's first partial row
-    {
-        const int i = threadIdx.x;              // E <= 256 = blockDim.x
-        const int tot_e = i < g.E ? ws.coltot[i] : 0;
-        int rows_total;
-        const int eoff = block_exclusive_scan(tot_e, wsum, &rows_total);
-        const int tot_d = i < g.R ? ws.coltot[g.E + i] : 0;
-        int recv_total;
-        const int doff = block_exclusive_scan(tot_d, wsum, &recv_total);
-        if (i < g.E) gbase[i] = cb[i] + eoff;
-        if (i < g.R) {
-            gbase[g.E + i] = cb[g.E + i];
-            roff[i] = doff;
-        }
-        if (i == 0) roff[g.R] = recv_total;
-        if (bid == 0) {
-            if (i < g.E) {
-                expert_counts[i] = tot_e;
-                expert_offsets[i] = eoff;
+    int er_i = -1, el_i = -1, tot_e = 0, tot_d = 0, cb_e = 0, cb_d = 0;
+    if (i < g.E) {
+        er_i = er[i];
+        el_i = el[i];
+        tot_e = ws.coltot[i];
+        cb_e = cb[i];
+    }
+    if (i < g.R) {
+        tot_d = ws.coltot[g.E + i];
+        cb_d = cb[g.E + i];
+    }
+    int t0, t1, src;
+    chunk_range(g, bid, t0, t1, src);
+    const int t = t0 + i;
+    const bool live = t < t1;
+    int e_raw[kMaxK];
+    uint8_t kp_raw[kMaxK];
+    uint64_t m = 0;
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s) {
+        e_raw[s] = -1;
+        kp_raw[s] = 0;
+    }
+    if (live) {
+        const size_t q0 = static_cast<size_t>(t) * g.k;
+#pragma unroll
+        for (int s = 0; s < kMaxK; ++s)
+            if (s < g.k) {
+                e_raw[s] = idx[q0 + s];
+                kp_raw[s] = keep[q0 + s];
             }
-            if (i == 0) expert_offsets[g.E] = rows_total;
-            if (i < g.R) recv_offsets[i] = doff;
-            if (i == 0) recv_offsets[g.R] = recv_total;
-            // send_counts[s][d] = rows of d from chunks of rank s
-            if (i < g.R) {
-                const int s = i;
+        m = device_bits(mask[t], g.R);
+    }
+    // block 0: send_counts[s][d] = rows of column E + d from the chunks of rank
+    // s = (base at rank s + 1's first chunk, or the total) - (base at rank s's)
+    // (every lane loads, clamped to the last pair, so that no branch splits
+    // the loads and they all go out before the first wait)
+    int sc[kSendPerThread];
+    if (bid == 0) {
+#pragma unroll
+        for (int j = 0; j < kSendPerThread; ++j) {
+            const int q = min(i + j * kChunk, g.R * g.R - 1);
+            const int s = q / g.R, d = q - s * g.R;
+            const int32_t* lp = ws.part + static_cast<size_t>(s * g.cpr * g.sub) * g.W + g.E + d;
+            const int32_t* hp = (s + 1 < g.R) ? lp + static_cast<size_t>(g.cpr * g.sub) * g.W : ws.coltot + g.E + d;
+            sc[j] = *hp - *lp;
+        }
+    }
+
+    // ---- LDS work
+    for (int k2 = i; k2 < kWavesPerChunk * g.W; k2 += blockDim.x) bits[k2 / g.W][k2 % g.W] = 0ull;
+    if (i < g.E) {
+        const bool ok = (static_cast<unsigned>(er_i) < static_cast<unsigned>(g.R)) &
+                        (static_cast<unsigned>(el_i) < static_cast<unsigned>(g.E_loc));
+        pos_lds[i] = ok ? er_i * g.E_loc + el_i : -1;
+    }
+    // expert offsets (slot-position order) and receive offsets from the column totals
+    int eoff, doff, rows_total, recv_total;
+    block_exclusive_scan2(tot_e, tot_d, wsum, eoff, doff, &rows_total, &recv_total);
+    if (i < g.E) gbase[i] = cb_e + eoff;
+    if (i < g.R) {
+        gbase[g.E + i] = cb_d;
+        roff[i] = doff;
+    }
+    if (i == 0) roff[g.R] = recv_total;
+    if (bid == 0) {
+        if (i < g.E) {
+            expert_counts[i] = tot_e;
+            expert_offsets[i] = eoff;
+        }
+        if (i == 0) expert_offsets[g.E] = rows_total;
+        if (i < g.R) recv_offsets[i] = doff;
+        if (i == 0) recv_offsets[g.R] = recv_total;
+#pragma unroll
+        for (int j = 0; j < kSendPerThread; ++j) {
+            const int q = i + j * kChunk;
+            if (q < g.R * g.R) sc_lds[q] = sc[j];
+        }
+        __syncthreads();
+        // send_offsets[s][d] = sum of send_counts[s][d'] over d' < d
+#pragma unroll
+        for (int j = 0; j < kSendPerThread; ++j) {
+            const int q = i + j * kChunk;
+            if (q < g.R * g.R) {
+                const int s = q / g.R, d = q - s * g.R;
                 int run = 0;
-                for (int d = 0; d < g.R; ++d) {
-                    const int lo = ws.part[static_cast<size_t>(s * g.cpr * g.sub) * g.W + g.E + d];
-                    const int hi = (s + 1 < g.R)
-                                       ? ws.part[static_cast<size_t>((s + 1) * g.cpr * g.sub) * g.W + g.E + d]
-                                       : ws.coltot[g.E + d];
-                    send_counts[s * g.R + d] = hi - lo;
-                    send_offsets[s * g.R + d] = run;
-                    run += hi - lo;
-                }
+                for (int d2 = 0; d2 < d; ++d2) run += sc_lds[s * g.R + d2];
+                send_counts[q] = sc[j];
+                send_offsets[q] = run;
             }
         }
     }
     __syncthreads();
 
-    int t0, t1, src;
-    chunk_range(g, bid, t0, t1, src);
-    const int t = t0 + threadIdx.x;
-    const bool live = t < t1;
     const unsigned long long me = 1ull << lane_id();
     int P[kMaxK];
-    uint64_t m = 0;
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s)
+        P[s] = (kp_raw[s] && static_cast<unsigned>(e_raw[s]) < static_cast<unsigned>(g.E)) ? pos_lds[e_raw[s]] : -1;
     if (live) {
-        load_token(g, t, idx, keep, mask, pos_lds, P, m);
 #pragma unroll
         for (int s = 0; s < kMaxK; ++s)
             if (P[s] >= 0) atomicOr(&bits[wave][P[s]], me);
