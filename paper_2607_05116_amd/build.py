@@ -31,12 +31,15 @@ CXXFLAGS = [
 ]
 
 
-# Per-file additions.  route_prune: its inputs are finite by contract, and
-# without NaN semantics the instruction selector does not re-derive NaN facts
-# through the long compare/select networks of the top-k (minutes -> seconds).
+# Per-file additions.  The routing kernels (route_prune, router_route and the
+# fused front end): their inputs are finite by contract, and without NaN
+# semantics the instruction selector neither re-derives NaN facts through the
+# long compare/select networks of the top-k (minutes -> seconds) nor quiets
+# the operands of every fp64 min/max of the packed-key networks.
 FILE_FLAGS = {
     "route_prune.hip": ["-fno-honor-nans"],
     "router_route.hip": ["-fno-honor-nans"],
+    "front_end.hip": ["-fno-honor-nans"],
 }
 
 

@@ -52,13 +52,16 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     __shared__ int pos_lds[kMaxE];
     __shared__ int hist[kRcWaves][kMaxW];
     __shared__ int vsum[4];
+    // expert tables in LDS, one entry per thread; their loads are issued
+    // together with the logit loads (no branch, so no early wait)
+    static_assert(kMaxE <= kRcThreads, "one table entry per thread");
+    const int e_me = min(static_cast<int>(threadIdx.x), g.E - 1);
+    const int er_v = expert_rank[e_me], el_v = expert_local[e_me];
     if (threadIdx.x < 4) vsum[threadIdx.x] = 0;
-    for (int e = threadIdx.x; e < g.E; e += blockDim.x) {
-        er_lds[e] = expert_rank[e] & 63;
-        pos_lds[e] = slot_position(expert_rank, expert_local, e, g);
-    }
     const int wave = threadIdx.x / kWave;
-    for (int i = threadIdx.x; i < kRcWaves * g.W; i += blockDim.x) hist[i / g.W][i % g.W] = 0;
+#pragma unroll
+    for (int w = 0; w < kRcWaves; ++w)
+        for (int i = threadIdx.x; i < g.W; i += blockDim.x) hist[w][i] = 0;
 
     // part h of chunk c
     const int sc = blockIdx.x;
@@ -97,6 +100,8 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
                 vals[c * CW + i] = row[e < g.E ? e : g.E - 1];
             }
     }
+    er_lds[threadIdx.x] = er_v & 63;               // entries past E are never read
+    pos_lds[threadIdx.x] = slot_position_of(er_v, el_v, g);
     __syncthreads();                               // er_lds, pos_lds, zeroed histograms ready
     const RouteResult res = route_token<V, K, VEC, false>(vals, lg, t, live, g.E, g.R, g.rpn, g.tpr,
                                                             inter_node_cost, p, er_lds, out_idx, out_w, out_keep,
@@ -121,17 +126,16 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     // n_inter, n_nodes, and their sums over the part (integer LDS adds)
     int v[4] = {0, 0, 0, 0};
     if (live && lg == 0) {
-        const int src_node = src / g.rpn;
-        uint64_t nodes = 0;
-        for (uint64_t b = m; b; b &= b - 1) {
+        // devices of one node: rpn consecutive bits; the source's node is `home`
+        const uint64_t node_bits = (g.rpn >= 64) ? ~0ull : ((1ull << g.rpn) - 1);
+        const uint64_t home = node_bits << ((src / g.rpn) * g.rpn);
+        v[0] = __popcll(m);
+        v[1] = __popcll(m & home & ~(1ull << src));
+        v[2] = __popcll(m & ~home);
+        for (uint64_t b = m; b; ++v[3]) {        // one step per node: drop all of its devices
             const int d = __ffsll(static_cast<unsigned long long>(b)) - 1;
-            ++v[0];
-            const int nd = d / g.rpn;
-            if (nd != src_node) ++v[2];
-            else if (d != src) ++v[1];
-            nodes |= 1ull << nd;
+            b &= ~(node_bits << (small_quotient(d, g.rpn) * g.rpn));
         }
-        v[3] = __popcll(nodes);
         reinterpret_cast<uint32_t*>(vol)[t] = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 8) |
                                               (static_cast<uint32_t>(v[2]) << 16) | (static_cast<uint32_t>(v[3]) << 24);
 #pragma unroll

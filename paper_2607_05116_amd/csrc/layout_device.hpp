@@ -33,14 +33,18 @@ __device__ __forceinline__ void chunk_range(const Geom& g, int c, int& t0, int& 
     t1 = min(t0 + kChunk, (src + 1) * g.tpr);
 }
 
+// Slot position r * E_loc + l of an expert on rank r at local index l, or -1
+// when the placement entry is out of range.
+__device__ __forceinline__ int slot_position_of(int r, int l, const Geom& g) {
+    const bool ok = (static_cast<unsigned>(r) < static_cast<unsigned>(g.R)) &
+                    (static_cast<unsigned>(l) < static_cast<unsigned>(g.E_loc));
+    return ok ? r * g.E_loc + l : -1;
+}
 // Both table entries are read before either is tested, so the two loads are
 // in flight together.
 __device__ __forceinline__ int slot_position(const int32_t* er, const int32_t* el, int e, const Geom& g) {
     if (static_cast<unsigned>(e) >= static_cast<unsigned>(g.E)) return -1;
-    const int r = er[e], l = el[e];
-    const bool ok = (static_cast<unsigned>(r) < static_cast<unsigned>(g.R)) &
-                    (static_cast<unsigned>(l) < static_cast<unsigned>(g.E_loc));
-    return ok ? r * g.E_loc + l : -1;
+    return slot_position_of(er[e], el[e], g);
 }
 
 __device__ __forceinline__ uint64_t device_bits(uint64_t m, int R) {

@@ -14,7 +14,7 @@ namespace {
 
 constexpr int kGroup = 8;              // lanes per token
 constexpr int kTokensPerBlock = 32;    // 256 threads
-constexpr double kNoKey = -1.0;        // below every packed key
+constexpr double kNoKey = -__builtin_inf();   // below every packed key
 
 // Gate exponential: Cody & Waite argument reduction with ln2 split as
 // LN2_HI (ln 2 to 16 significant bits, exact products n*LN2_HI for |n| < 2^8)
@@ -37,24 +37,29 @@ __device__ __forceinline__ float gate_exp(float z) {
     return (z >= -87.33f) ? e : 0.0f;
 }
 
-// Order-preserving image of a float (total order on non-NaN values).
-__device__ __forceinline__ uint32_t ordered_bits(float x) {
-    const uint32_t b = __float_as_uint(x + 0.0f);   // -0.0 -> +0.0
-    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-__device__ __forceinline__ float from_ordered_bits(uint32_t u) {
-    return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
-}
-
-__device__ __forceinline__ double pack_key(float x, int e) {
-    const uint64_t k = (static_cast<uint64_t>(ordered_bits(x)) << 30) | static_cast<uint64_t>(255 - e);
-    return __longlong_as_double(static_cast<long long>(k));
+// Selection key of (logit x, expert e): the fp64 whose high word is the bits
+// of x (with -0.0 folded to +0.0) and whose low word is 255 - e, with all 32
+// bits of the low word complemented when x is negative.  fp64 order on such keys is the selection
+// order: sign and magnitude of the high word order the logits as fp32 order
+// does, and within one logit the low word puts the lower expert first on
+// either side of zero (complementing reverses the order of the magnitudes of
+// negative keys).  No key is NaN or infinite for finite logits; keys of 0.0
+// and of tiny subnormal logits are fp64 subnormals, compared exactly because
+// fp64 denormals are not flushed.
+__device__ __forceinline__ double pack_key(float x, uint32_t tie_g, uint32_t tie_c) {
+    const uint32_t hi = __float_as_uint(x + 0.0f);
+    uint32_t lo;
+    // lo = sign mask ^ tie_g ^ tie_c in one three-input bit op (truth table 0x96)
+    asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(lo) : "v"(static_cast<int32_t>(hi) >> 31), "v"(tie_g), "s"(tie_c));
+    return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
 }
 __device__ __forceinline__ int key_expert(double k) {
-    return 255 - static_cast<int>(static_cast<uint64_t>(__double_as_longlong(k)) & 255u);
+    const uint64_t b = static_cast<uint64_t>(__double_as_longlong(k));
+    const uint32_t lo = static_cast<uint32_t>(b) ^ static_cast<uint32_t>(static_cast<int32_t>(b >> 32) >> 31);
+    return 255 - static_cast<int>(lo & 255u);
 }
 __device__ __forceinline__ float key_logit(double k) {
-    return from_ordered_bits(static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(k)) >> 30));
+    return __uint_as_float(static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(k)) >> 32));
 }
 
 // Descending compare-exchange.
@@ -65,24 +70,21 @@ __device__ __forceinline__ void cx(double& a, double& b) {
     b = lo;
 }
 
-// Bitonic sort (descending) of N = 2^m keys.
+// Descending sort of N = 2^m keys by Batcher's odd-even merge sort (Knuth,
+// TAOCP vol. 3, Sec. 5.3.4): runs of length 2p are merged from sorted halves,
+// comparing at distance k = p, p/2, ..., 1 only inside each run; 19
+// compare-exchanges for N = 8, against 24 for the bitonic sorter.
 template <int N>
-__device__ __forceinline__ void bitonic_sort(double (&v)[N]) {
+__device__ __forceinline__ void sort_desc(double (&v)[N]) {
 #pragma unroll
-    for (int size = 2; size <= N; size <<= 1) {
+    for (int p = 1; p < N; p <<= 1)
 #pragma unroll
-        for (int stride = size / 2; stride >= 1; stride >>= 1) {
+        for (int k = p; k >= 1; k >>= 1)
 #pragma unroll
-            for (int i = 0; i < N; ++i) {
-                const int j = i ^ stride;
-                if (j > i) {
-                    // descending within blocks whose (i & size) == 0, ascending otherwise
-                    if ((i & size) == 0) cx(v[i], v[j]);
-                    else cx(v[j], v[i]);
-                }
-            }
-        }
-    }
+            for (int j = k % p; j + k < N; j += 2 * k)
+#pragma unroll
+                for (int i = 0; i < k; ++i)
+                    if (i + j + k < N && (i + j) / (2 * p) == (i + j + k) / (2 * p)) cx(v[i + j], v[i + j + k]);
 }
 
 // a := top N of (a, b), both sorted descending; result sorted descending.
@@ -103,8 +105,8 @@ __device__ __forceinline__ void merge_top(double (&a)[N], const double (&b)[N]) 
 template <int CTRL>
 __device__ __forceinline__ double dpp_swap(double v) {
     const long long b = __double_as_longlong(v);
-    const int lo = __builtin_amdgcn_update_dpp(0, static_cast<int>(b), CTRL, 0xF, 0xF, false);
-    const int hi = __builtin_amdgcn_update_dpp(0, static_cast<int>(b >> 32), CTRL, 0xF, 0xF, false);
+    const int lo = __builtin_amdgcn_mov_dpp(static_cast<int>(b), CTRL, 0xF, 0xF, true);
+    const int hi = __builtin_amdgcn_mov_dpp(static_cast<int>(b >> 32), CTRL, 0xF, 0xF, true);
     return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<uint32_t>(lo));
 }
 constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
@@ -133,15 +135,37 @@ __device__ __forceinline__ float group_lane(float v) {
 }
 
 // One step of a descending sort across the 8 lanes: the lane that is `lower`
-// in its pair keeps the larger (key, a), the other keeps the smaller.
+// in its pair keeps the larger (key, a), the other keeps the smaller.  Keys
+// are distinct except kNoKey, whose a is never read.
 template <int CTRL>
 __device__ __forceinline__ void lane_cx(double& key, float& a, bool lower) {
     const double pk = dpp_swap<CTRL>(key);
-    const float pa = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), CTRL, 0xF, 0xF, false));
-    const bool take = lower ? (pk > key) : (pk < key);
-    key = take ? pk : key;
-    a = take ? pa : a;
+    const float pa = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(a), CTRL, 0xF, 0xF, true));
+    const double nk = lower ? __builtin_fmax(key, pk) : __builtin_fmin(key, pk);
+    a = (nk == key) ? a : pa;
+    key = nk;
 }
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_swap_u64(uint64_t v) {
+    return static_cast<uint64_t>(__double_as_longlong(dpp_swap<CTRL>(__longlong_as_double(static_cast<long long>(v)))));
+}
+
+// Lanes of a wave whose position g in their 8-lane group is above s.
+__device__ __forceinline__ constexpr uint64_t lanes_after_slot(int s) {
+    return 0x0101010101010101ull * ((0xFFull << (s + 1)) & 0xFFull);
+}
+
+// floor(n / d) for 0 <= n < 2^31 and 1 <= d < 2^31 with a quotient below
+// 2^16: the fp32 estimate n * rcp(d) is within 2^-21 of n / d relative (so
+// within one of the quotient), and one correction step each way makes it exact.
+__device__ __forceinline__ int small_quotient(int n, int d) {
+    int q = static_cast<int>(static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(d)));
+    const long long r = static_cast<long long>(n) - static_cast<long long>(q) * d;
+    q += (r >= d) ? 1 : 0;
+    q -= (r < 0) ? 1 : 0;
+    return q;
+}
+
 constexpr int kDppMirror4 = 0x1B;       // quad_perm [3,2,1,0]
 
 // What a lane knows of its token after the decision: the expert of its slot
@@ -165,13 +189,17 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
                                                    uint64_t* __restrict__ out_mask) {
     constexpr int KP = pow2_at_least(K);
     constexpr int CW = V < 4 ? V : 4;
+    // 255 - e = 255 ^ e, and e = c * 8 * CW + g * CW + i sums disjoint bit
+    // fields, so the tie word is a lane term xor a constant
+    const uint32_t tie_g = 255u ^ static_cast<uint32_t>(g * CW);
     double keys[V];
 #pragma unroll
     for (int c = 0; c < V / CW; ++c)
 #pragma unroll
         for (int i = 0; i < CW; ++i) {
             const int e = c * (kGroup * CW) + g * CW + i;
-            keys[c * CW + i] = (VEC || e < E) ? pack_key(vals[c * CW + i], e) : kNoKey;
+            keys[c * CW + i] = (VEC || e < E) ? pack_key(vals[c * CW + i], tie_g, static_cast<uint32_t>(c * (kGroup * CW) + i))
+                                              : kNoKey;
         }
 
     // ---- lane-local top KP: sort blocks of KP keys, merge them
@@ -180,13 +208,13 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
         constexpr int B = V < KP ? V : KP;     // keys per block
 #pragma unroll
         for (int s = 0; s < KP; ++s) top[s] = s < B ? keys[s] : kNoKey;
-        bitonic_sort<KP>(top);
+        sort_desc<KP>(top);
 #pragma unroll
         for (int b0 = KP; b0 < V; b0 += KP) {
             double blk[KP];
 #pragma unroll
             for (int s = 0; s < KP; ++s) blk[s] = keys[b0 + s];
-            bitonic_sort<KP>(blk);
+            sort_desc<KP>(blk);
             merge_top<KP>(top, blk);
         }
     }
@@ -215,48 +243,56 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
     CAP_GATHER_SLOT(0) CAP_GATHER_SLOT(1) CAP_GATHER_SLOT(2) CAP_GATHER_SLOT(3)
     CAP_GATHER_SLOT(4) CAP_GATHER_SLOT(5) CAP_GATHER_SLOT(6) CAP_GATHER_SLOT(7)
 #undef CAP_GATHER_SLOT
-    float S = 0.0f;
+    float S = qs[0];
 #pragma unroll
-    for (int s = 0; s < K; ++s) S = S + qs[s];
-    float ws[K];                               // every slot's gate, on every lane
-#pragma unroll
-    for (int s = 0; s < K; ++s) ws[s] = qs[s] / S;
+    for (int s = 1; s < K; ++s) S = S + qs[s];
+    // lane g divides for its own slot; every lane then takes every slot's gate
+    const float my_w = q / S;
+    float ws[K];
+#define CAP_GATHER_GATE(S_) \
+    if constexpr (S_ < K) ws[S_] = group_lane<S_>(my_w);
+    CAP_GATHER_GATE(0) CAP_GATHER_GATE(1) CAP_GATHER_GATE(2) CAP_GATHER_GATE(3)
+    CAP_GATHER_GATE(4) CAP_GATHER_GATE(5) CAP_GATHER_GATE(6) CAP_GATHER_GATE(7)
+#undef CAP_GATHER_GATE
 
-    // ---- pruning
+    // ---- pruning: a prefix of a ranked list is kept; each lane sets the bit of
+    // the device it ranks, and the group ORs the bits together
     const float target = 1.0f - p;
     const bool keep_all = (p == 0.0f);
-    uint64_t mask = 0;
-    float Sk = 0.0f;
-    int n_keep = K;                         // naive: slots kept (a prefix)
+    bool rank_kept;                         // the device this lane ranks is kept
+    int rank_dev;
+    bool slot_kept = false;                 // naive: slot g is in the kept prefix
     if constexpr (NAIVE) {
         // expert level: the shortest slot prefix whose running score reaches 1 - p
-        float cum = 0.0f;
+        float cum = ws[0];
+        int n_keep = (!keep_all && cum >= target) ? 1 : K;
 #pragma unroll
-        for (int s = 0; s < K; ++s) {
+        for (int s = 1; s < K; ++s) {
             cum = cum + ws[s];
-            if (!keep_all && n_keep == K && cum >= target) n_keep = s + 1;
+            n_keep = (n_keep == K && !keep_all && cum >= target) ? s + 1 : n_keep;
         }
-#pragma unroll
-        for (int s = 0; s < K; ++s) {
-            if (s < n_keep) mask |= 1ull << devs[s];
-            Sk = Sk + ((s < n_keep) ? ws[s] : 0.0f);
-        }
+        rank_kept = has_slot && g < n_keep;
+        slot_kept = rank_kept;
+        rank_dev = my_dev & 63;
     } else {
-        const int src = (live ? t : 0) / tokens_per_rank;
-        const int src_node = src / ranks_per_node;
-        // lane g is a candidate if slot g is the first slot of its device;
-        // a = that device's score summed in slot order
-        bool cand = has_slot;
+        const int src = small_quotient(live ? t : 0, tokens_per_rank);
+        // lane g is a candidate if slot g is the first slot of its device
+        // (no earlier slot on the same device: a lane mask built from ballots);
+        // a = that device's score summed in slot order (earlier slots add +0)
+        uint64_t repeat = 0;
         float a = 0.0f;
 #pragma unroll
         for (int s = 0; s < K; ++s) {
             const bool same = devs[s] == my_dev;
-            if (s < g) cand = cand && !same;
-            a = a + ((s >= g && same) ? ws[s] : 0.0f);
+            a = a + (same ? ws[s] : 0.0f);
+            repeat |= __builtin_amdgcn_ballot_w64(same) & lanes_after_slot(s);
         }
+        const bool cand = has_slot && !__builtin_amdgcn_inverse_ballot_w64(repeat);
         float ratio = a;
         if (my_dev == src) ratio = INFINITY;
-        else if (R > ranks_per_node && my_dev / ranks_per_node != src_node) ratio = a / inter_node_cost;
+        else if (R > ranks_per_node &&
+                 small_quotient(my_dev, ranks_per_node) != small_quotient(src, ranks_per_node))
+            ratio = a / inter_node_cost;
         const uint64_t kbits = (1ull << 61) | (static_cast<uint64_t>(__float_as_uint(ratio)) << 30) |
                                (static_cast<uint64_t>(63 - (my_dev & 63)) << 3);
         double ck = cand ? __longlong_as_double(static_cast<long long>(kbits)) : kNoKey;
@@ -268,33 +304,39 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
         lane_cx<kDppHalfMirror>(ck, ca, g < 4);
         lane_cx<kDppXor2>(ck, ca, (g & 2) == 0);
         lane_cx<kDppXor1>(ck, ca, (g & 1) == 0);
-        // greedy retention in key order, replayed by every lane
-        const uint32_t ck_hi = static_cast<uint32_t>(static_cast<uint64_t>(__double_as_longlong(ck)) >> 32);
-        const int ck_lo = static_cast<int>(static_cast<uint64_t>(__double_as_longlong(ck)));
-        float cum = 0.0f;
-        bool done = false;
-#define CAP_GREEDY_STEP(S_)                                                          \
-        if constexpr (S_ < K) {                                                          \
-            const bool c2 = (group_lane<S_>(static_cast<int>(ck_hi)) >> 29) == 1;        \
-            const float a2 = group_lane<S_>(ca);                                         \
-            const int d2 = 63 - ((group_lane<S_>(ck_lo) >> 3) & 63);                     \
-            if (c2 && (keep_all || !done)) mask |= 1ull << d2;                           \
-            cum = cum + (c2 ? a2 : 0.0f);                                                \
-            done = done || (c2 && cum >= target);                                        \
+        // greedy retention in key order, replayed by every lane: the running
+        // sum over the ranked candidates (non-candidates rank last and add +0,
+        // so they can neither change the sum nor be the first to reach 1 - p)
+        const uint64_t ckb = static_cast<uint64_t>(__double_as_longlong(ck));
+        const bool ranked = (static_cast<uint32_t>(ckb >> 32) >> 29) == 1u;
+        const float ra = ranked ? ca : 0.0f;
+        float cum = group_lane<0>(ra);
+        int n_keep = (cum >= target) ? 1 : K;
+#define CAP_GREEDY_STEP(S_)                                                   \
+        if constexpr (S_ > 0 && S_ < K) {                                         \
+            cum = cum + group_lane<S_>(ra);                                       \
+            n_keep = (n_keep == K && cum >= target) ? S_ + 1 : n_keep;            \
         }
-        CAP_GREEDY_STEP(0) CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
+        CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
         CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6) CAP_GREEDY_STEP(7)
 #undef CAP_GREEDY_STEP
-#pragma unroll
-        for (int s = 0; s < K; ++s) Sk = Sk + (((mask >> devs[s]) & 1ull) ? ws[s] : 0.0f);
+        rank_kept = ranked && (keep_all || g < n_keep);
+        rank_dev = 63 - static_cast<int>((ckb >> 3) & 63u);
     }
+    uint64_t mask = rank_kept ? (1ull << rank_dev) : 0ull;
+    mask |= dpp_swap_u64<kDppXor1>(mask);
+    mask |= dpp_swap_u64<kDppXor2>(mask);
+    mask |= dpp_swap_u64<kDppHalfMirror>(mask);
 
-    // ---- lane g writes slot g
-    const bool my_keep = has_slot && (NAIVE ? (g < n_keep) : ((mask >> (my_dev & 63)) & 1ull));
+    // ---- S' = kept gates summed in slot order; lane g writes slot g
+    const bool my_keep = NAIVE ? slot_kept : has_slot && ((mask >> (my_dev & 63)) & 1ull);
+    const float kw = my_keep ? my_w : 0.0f;
+    float Sk = group_lane<0>(kw);
+#define CAP_KEPT_SUM(S_) \
+    if constexpr (S_ > 0 && S_ < K) Sk = Sk + group_lane<S_>(kw);
+    CAP_KEPT_SUM(1) CAP_KEPT_SUM(2) CAP_KEPT_SUM(3) CAP_KEPT_SUM(4) CAP_KEPT_SUM(5) CAP_KEPT_SUM(6) CAP_KEPT_SUM(7)
+#undef CAP_KEPT_SUM
     if (live && has_slot) {
-        float my_w = ws[0];
-#pragma unroll
-        for (int s = 1; s < K; ++s) my_w = (g == s) ? ws[s] : my_w;
         const size_t qi = static_cast<size_t>(t) * K + g;
         out_idx[qi] = my_e;
         out_w[qi] = my_keep ? my_w / Sk : 0.0f;

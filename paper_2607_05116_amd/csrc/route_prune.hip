@@ -50,8 +50,11 @@ __global__ __launch_bounds__(256) void route_prune_kernel(
     int tokens_per_rank, float inter_node_cost, float p,
     const int32_t* __restrict__ expert_rank, int32_t* __restrict__ out_idx,
     float* __restrict__ out_w, uint8_t* __restrict__ out_keep, uint64_t* __restrict__ out_mask) {
+    // expert -> rank table in LDS, one entry per thread; its load is issued
+    // together with the logit loads so that neither waits for the other
+    static_assert(kMaxE <= kTokensPerBlock * kGroup, "one table entry per thread");
     __shared__ int er_lds[kMaxE];
-    for (int e = threadIdx.x; e < E; e += blockDim.x) er_lds[e] = expert_rank[e] & 63;
+    const int er_v = expert_rank[min(static_cast<int>(threadIdx.x), E - 1)];   // no branch: no early wait
 
     const int g = threadIdx.x & (kGroup - 1);
     const int t = blockIdx.x * kTokensPerBlock + (threadIdx.x >> 3);
@@ -84,6 +87,7 @@ __global__ __launch_bounds__(256) void route_prune_kernel(
                 vals[c * CW + i] = row[e < E ? e : E - 1];
             }
     }
+    er_lds[threadIdx.x] = er_v & 63;           // entries past E are never read
     __syncthreads();                           // er_lds ready
     route_token<V, K, VEC, NAIVE>(vals, g, t, live, E, R, ranks_per_node, tokens_per_rank, inter_node_cost, p,
                                   er_lds, out_idx, out_w, out_keep, out_mask);

@@ -308,6 +308,12 @@ def _adversarial_logits(T, E, seed):
     L[T // 4: T // 4 + 8] = 0.0                                                    # all equal
     L[T // 4 + 8: T // 4 + 16] = -0.0
     L[T // 4 + 16: T // 4 + 24, ::2] = -0.0                                        # +-0 mix
+    tiny = np.array([1e-45, 1e-40, 1e-38, 0.0, -0.0, -1e-45, -1e-40, -1e-38], np.float32)
+    huge = np.array([8.5e37, 3e36, 1e30, -1e30, -3e36, -8.5e37], np.float32)
+    blk = L[T // 4 + 24: T // 4 + 32]
+    blk[:] = rng.choice(tiny, size=blk.shape)                                      # subnormal ties
+    blk = L[T // 4 + 32: T // 4 + 40]
+    blk[:] = rng.choice(huge, size=blk.shape)                                      # extreme exponents
     return L
 
 
