@@ -223,10 +223,16 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
     merge_with_partner<kDppXor2, KP>(top);
     merge_with_partner<kDppHalfMirror, KP>(top);
 
-    // ---- lane g owns slot g (lanes g >= K own nothing)
-    double mine = top[0];
+    // ---- lane g owns slot g (lanes g >= K own nothing): top[g mod KP] by a
+    // select on each bit of g
+    double sel[KP];
 #pragma unroll
-    for (int s = 1; s < KP; ++s) mine = (g == s) ? top[s] : mine;
+    for (int s = 0; s < KP; ++s) sel[s] = top[s];
+#pragma unroll
+    for (int half = KP / 2, bit = 0; half >= 1; half >>= 1, ++bit)
+#pragma unroll
+        for (int i = 0; i < half; ++i) sel[i] = ((g >> bit) & 1) ? sel[2 * i + 1] : sel[2 * i];
+    const double mine = sel[0];
     const bool has_slot = g < K;
     const int my_e = key_expert(mine);
     const int my_dev = has_slot ? er_lds[my_e < E ? my_e : 0] : -1;
@@ -309,18 +315,20 @@ __device__ __forceinline__ RouteResult route_token(const float (&vals)[V], int g
         // so they can neither change the sum nor be the first to reach 1 - p)
         const uint64_t ckb = static_cast<uint64_t>(__double_as_longlong(ck));
         const bool ranked = (static_cast<uint32_t>(ckb >> 32) >> 29) == 1u;
+        // The sum never decreases, so the first rank at which it reaches 1 - p
+        // is the number of earlier ranks at which it was still below.
         const float ra = ranked ? ca : 0.0f;
         float cum = group_lane<0>(ra);
-        int n_keep = (cum >= target) ? 1 : K;
+        int below = (cum < target) ? 1 : 0;
 #define CAP_GREEDY_STEP(S_)                                                   \
-        if constexpr (S_ > 0 && S_ < K) {                                         \
+        if constexpr (S_ > 0 && S_ < K - 1) {                                     \
             cum = cum + group_lane<S_>(ra);                                       \
-            n_keep = (n_keep == K && cum >= target) ? S_ + 1 : n_keep;            \
+            below += (cum < target) ? 1 : 0;                                      \
         }
         CAP_GREEDY_STEP(1) CAP_GREEDY_STEP(2) CAP_GREEDY_STEP(3)
-        CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6) CAP_GREEDY_STEP(7)
+        CAP_GREEDY_STEP(4) CAP_GREEDY_STEP(5) CAP_GREEDY_STEP(6)
 #undef CAP_GREEDY_STEP
-        rank_kept = ranked && (keep_all || g < n_keep);
+        rank_kept = ranked && (keep_all || g <= below);   // ranks 0 .. first reaching rank
         rank_dev = 63 - static_cast<int>((ckb >> 3) & 63u);
     }
     uint64_t mask = rank_kept ? (1ull << rank_dev) : 0ull;

@@ -13,26 +13,30 @@
 //   greedy running sum in key order (ties: lower device id), stop at >= 1 - p
 //   w'_s   = w_s / S' over kept slots (S' summed in slot order).
 //
-// Selection keys.  A (logit, expert) pair is packed into one positive fp64
-// whose order is the selection order (logit descending, then expert id
-// ascending): bits 61..30 hold the logit's order-preserving 32-bit image and
-// bits 7..0 hold 255 - expert.  Such a double is never NaN or infinite and,
-// for every finite logit, is a normal number, so v_max_f64 / v_min_f64 compare
-// it exactly; a compare-exchange is then two branch-free instructions.  -0.0
-// is folded to +0.0 first, because the two compare equal as logits (the tie
-// then goes to the lower expert id, as for any other equal pair).
+// Selection keys.  A (logit, expert) pair is packed into one fp64 whose order
+// is the selection order (logit descending, then expert id ascending): the
+// high word is the logit's own bits, so fp64 sign-magnitude order matches fp32
+// order, and the low word is 255 - expert, complemented for negative logits
+// (whose fp64 magnitudes order in reverse).  Such a double is never NaN or
+// infinite; zero and tiny logits give fp64 subnormals, which are not flushed,
+// so v_max_f64 / v_min_f64 compare every key exactly and a compare-exchange is
+// two branch-free instructions.  -0.0 is folded to +0.0 first, because the two
+// compare equal as logits (the tie then goes to the lower expert id, as for
+// any other equal pair).
 //
 // Layout: 8 lanes cooperate on one token (8 tokens per wave).  Lane j holds V
 // logits of the row (loaded as 16-byte vectors, so a group reads the row in
-// contiguous 128-byte pieces), sorts them in blocks of KP = pow2 >= k with a
-// bitonic network and keeps the top KP; three butterfly merges across the
-// group (DPP lane swaps) leave every lane with the token's sorted top KP.
-// From there lane j owns slot j: it computes its own gate exponential and
-// takes the slot-ordered sums (S, a_d, S') from the group's lanes through
+// contiguous 128-byte pieces), sorts them in blocks of KP = pow2 >= k with
+// Batcher's odd-even merge sort and keeps the top KP (bitonic merges of the
+// sorted blocks); three butterfly merges across the group (DPP lane swaps)
+// leave every lane with the token's sorted top KP.  From there lane j owns
+// slot j: it computes its own gate exponential and gate division and takes
+// the slot-ordered sums (S, a_d, S') from the group's lanes through
 // ds_swizzle broadcasts, so every sum keeps its sequential order.  The
 // candidate devices (one lane each) are sorted across the group with the same
-// packed-double network, and each lane replays the greedy over the sorted
-// list to build the device mask.
+// kind of packed-double keys; every lane replays the greedy's running sum over
+// the ranked list, which fixes how many of the ranked devices are kept, and
+// the group ORs the kept devices' bits into the mask.
 #pragma clang fp contract(off)
 
 #include <math.h>
