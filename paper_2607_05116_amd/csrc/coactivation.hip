@@ -16,13 +16,14 @@
 //   2. reduce  every packed word summed over the splits (split groups in
 //              parallel, then a fixed-order LDS sum), unpacked and written to
 //              (i, j) and (j, i), added to C when accumulating.
-// Workspace: [S][ceil(E(E+1)/4)] uint32 packed partials.
+// Workspace: [S][4 * ceil(ceil(E(E+1)/4) / 4)] uint32 packed partials (each
+// split's slab padded to whole 16-byte quads).
 #include "coact_device.hpp"
 
 namespace cap {
 
 size_t coact_workspace_bytes(int T, int E) {
-    return static_cast<size_t>(coact_splits(T)) * tri_words(E) * sizeof(uint32_t);
+    return coact_part_bytes(T, E);
 }
 
 cap_status coactivation_launch(int T, int k, int E, const int32_t* idx, const uint8_t* keep, uint32_t* coact,

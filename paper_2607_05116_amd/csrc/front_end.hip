@@ -194,7 +194,7 @@ Front front_carve(const cap_topology* tp, void* base) {
     f.ws = carve(f.g, base, &lay);
     lay = align256(lay);
     f.coact_part = reinterpret_cast<uint32_t*>(static_cast<char*>(base) + lay);
-    f.bytes = lay + static_cast<size_t>(coact_splits(tp->T)) * tri_words(tp->E) * sizeof(uint32_t);
+    f.bytes = lay + coact_part_bytes(tp->T, tp->E);
     return f;
 }
 
