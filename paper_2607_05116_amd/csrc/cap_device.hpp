@@ -54,6 +54,17 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
     return l == 0 ? 0ull : (~0ull >> (64 - l));
 }
 
+// floor(n / d) for 0 <= n < 2^31 and 1 <= d < 2^31 with a quotient below
+// 2^16: the fp32 estimate n * rcp(d) is within 2^-21 of n / d relative (so
+// within one of the quotient), and one correction step each way makes it exact.
+__device__ __forceinline__ int small_quotient(int n, int d) {
+    int q = static_cast<int>(static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(d)));
+    const long long r = static_cast<long long>(n) - static_cast<long long>(q) * d;
+    q += (r >= d) ? 1 : 0;
+    q -= (r < 0) ? 1 : 0;
+    return q;
+}
+
 // Grid-wide launch helpers: compute units and XCDs of the current device.
 int device_cu_count();
 int device_xcc_count();

@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     const int wave = threadIdx.x / kWave;
 #pragma unroll
     for (int w = 0; w < kRcWaves; ++w)
-        for (int i = threadIdx.x; i < g.W; i += blockDim.x) hist[w][i] = 0;
+        for (int i = threadIdx.x; i < g.W; i += kRcThreads) hist[w][i] = 0;
 
     // part h of chunk c
     const int sc = blockIdx.x;
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     __syncthreads();
     if (threadIdx.x < 4) ws.volpart[sc * 4 + threadIdx.x] = vsum[threadIdx.x];
     int32_t* out = ws.part + static_cast<size_t>(sc) * g.W;
-    for (int col = threadIdx.x; col < g.W; col += blockDim.x) {
+    for (int col = threadIdx.x; col < g.W; col += kRcThreads) {
         int s = 0;
 #pragma unroll
         for (int w = 0; w < kRcWaves; ++w) s += hist[w][col];

@@ -110,8 +110,8 @@ __global__ __launch_bounds__(kChunk) void layout_count_kernel(
     __shared__ int cnt[kMaxW];
     __shared__ int pos_lds[kMaxE];
     __shared__ int vsum[kWavesPerChunk][4];
-    for (int i = threadIdx.x; i < g.W; i += blockDim.x) cnt[i] = 0;
-    for (int e = threadIdx.x; e < g.E; e += blockDim.x) pos_lds[e] = slot_position(er, el, e, g);
+    for (int i = threadIdx.x; i < g.W; i += kChunk) cnt[i] = 0;
+    for (int e = threadIdx.x; e < g.E; e += kChunk) pos_lds[e] = slot_position(er, el, e, g);
     __syncthreads();
 
     int t0, t1, src;
@@ -147,7 +147,7 @@ __global__ __launch_bounds__(kChunk) void layout_count_kernel(
     }
     __syncthreads();
     int32_t* out = ws.part + static_cast<size_t>(blockIdx.x) * g.W;
-    for (int i = threadIdx.x; i < g.W; i += blockDim.x) out[i] = cnt[i];
+    for (int i = threadIdx.x; i < g.W; i += kChunk) out[i] = cnt[i];
     if (threadIdx.x < 4) {
         int64_t s = 0;
 #pragma unroll
@@ -248,7 +248,7 @@ __device__ __forceinline__ void block_exclusive_scan2(int a, int b, int (*wsum)[
 // for one round of memory latency before its LDS work: the placement tables,
 // the column totals, the chunk's column bases, the token's slots and mask, and
 // in block 0 the rank-boundary bases that give send_counts (send_offsets then
-// come from a per-rank scan in LDS).
+// come from one block scan over the (s, d) pairs).
 constexpr int kSendPerThread = kMaxR * kMaxR / kChunk;   // (s, d) pairs per thread in block 0
 static_assert(kMaxR * kMaxR % kChunk == 0, "send-count pairs split evenly over the block");
 
@@ -266,62 +266,63 @@ __device__ __forceinline__ void layout_scatter_block(
     __shared__ int32_t roff[kMaxR + 1];
     __shared__ int wsum[2][kWavesPerChunk];
     __shared__ int32_t sc_lds[kMaxR * kMaxR];
-    const int i = threadIdx.x;                  // E <= 256 = blockDim.x
+    const int i = threadIdx.x;                  // E <= 256 = kChunk threads
     const int wave = i / kWave;
 
-    // ---- one round of independent loads
+    // ---- one round of independent loads (indices clamped rather than tested,
+    // so that no branch splits the loads and they all go out before the first
+    // wait; what a clamped lane loaded is dropped after the wait)
     const int32_t* cb = ws.part + static_cast<size_t>(bid) * g.sub * g.W;     // the chunk's first partial row
-    int er_i = -1, el_i = -1, tot_e = 0, tot_d = 0, cb_e = 0, cb_d = 0;
-    if (i < g.E) {
-        er_i = er[i];
-        el_i = el[i];
-        tot_e = ws.coltot[i];
-        cb_e = cb[i];
-    }
-    if (i < g.R) {
-        tot_d = ws.coltot[g.E + i];
-        cb_d = cb[g.E + i];
-    }
+    const int ie = min(i, g.E - 1), ir = min(i, g.R - 1);
+    int er_i = er[ie], el_i = el[ie], tot_e = ws.coltot[ie], cb_e = cb[ie];
+    int tot_d = ws.coltot[g.E + ir], cb_d = cb[g.E + ir];
     int t0, t1, src;
     chunk_range(g, bid, t0, t1, src);
     const int t = t0 + i;
     const bool live = t < t1;
+    const int tc = min(t, t1 - 1);              // chunks are never empty
     int e_raw[kMaxK];
     uint8_t kp_raw[kMaxK];
-    uint64_t m = 0;
+    {
+        const size_t q0 = static_cast<size_t>(tc) * g.k;
 #pragma unroll
-    for (int s = 0; s < kMaxK; ++s) {
-        e_raw[s] = -1;
-        kp_raw[s] = 0;
+        for (int s = 0; s < kMaxK; ++s) {
+            const size_t q = q0 + min(s, g.k - 1);
+            e_raw[s] = idx[q];
+            kp_raw[s] = keep[q];
+        }
     }
-    if (live) {
-        const size_t q0 = static_cast<size_t>(t) * g.k;
-#pragma unroll
-        for (int s = 0; s < kMaxK; ++s)
-            if (s < g.k) {
-                e_raw[s] = idx[q0 + s];
-                kp_raw[s] = keep[q0 + s];
-            }
-        m = device_bits(mask[t], g.R);
-    }
+    const uint64_t m_raw = mask[tc];
     // block 0: send_counts[s][d] = rows of column E + d from the chunks of rank
     // s = (base at rank s + 1's first chunk, or the total) - (base at rank s's)
-    // (every lane loads, clamped to the last pair, so that no branch splits
-    // the loads and they all go out before the first wait)
-    int sc[kSendPerThread];
+    // (thread i takes the consecutive pairs q = i * kSendPerThread + j, those
+    // past R * R clamped to the last one)
+    int sc_hi[kSendPerThread], sc_lo[kSendPerThread];
     if (bid == 0) {
 #pragma unroll
         for (int j = 0; j < kSendPerThread; ++j) {
-            const int q = min(i + j * kChunk, g.R * g.R - 1);
-            const int s = q / g.R, d = q - s * g.R;
+            const int q = min(i * kSendPerThread + j, g.R * g.R - 1);
+            const int s = small_quotient(q, g.R), d = q - s * g.R;
             const int32_t* lp = ws.part + static_cast<size_t>(s * g.cpr * g.sub) * g.W + g.E + d;
             const int32_t* hp = (s + 1 < g.R) ? lp + static_cast<size_t>(g.cpr * g.sub) * g.W : ws.coltot + g.E + d;
-            sc[j] = *hp - *lp;
+            sc_hi[j] = *hp;
+            sc_lo[j] = *lp;
         }
     }
 
     // ---- LDS work
-    for (int k2 = i; k2 < kWavesPerChunk * g.W; k2 += blockDim.x) bits[k2 / g.W][k2 % g.W] = 0ull;
+#pragma unroll
+    for (int w = 0; w < kWavesPerChunk; ++w)
+        for (int c = i; c < g.W; c += kChunk) bits[w][c] = 0ull;
+    if (i >= g.E) tot_e = 0;
+    if (i >= g.R) tot_d = 0;
+#pragma unroll
+    for (int s = 0; s < kMaxK; ++s)
+        if (!live || s >= g.k) {
+            e_raw[s] = -1;
+            kp_raw[s] = 0;
+        }
+    const uint64_t m = live ? device_bits(m_raw, g.R) : 0ull;
     if (i < g.E) {
         const bool ok = (static_cast<unsigned>(er_i) < static_cast<unsigned>(g.R)) &
                         (static_cast<unsigned>(el_i) < static_cast<unsigned>(g.E_loc));
@@ -344,22 +345,35 @@ __device__ __forceinline__ void layout_scatter_block(
         if (i == 0) expert_offsets[g.E] = rows_total;
         if (i < g.R) recv_offsets[i] = doff;
         if (i == 0) recv_offsets[g.R] = recv_total;
+        // send_offsets[s][d] = sum of send_counts[s][d'] over d' < d: the
+        // exclusive scan over all pairs in row-major order, less its value at
+        // the row's first pair
+        const int nq = g.R * g.R;
+        int sc[kSendPerThread];
+#pragma unroll
+        for (int j = 0; j < kSendPerThread; ++j) sc[j] = sc_hi[j] - sc_lo[j];
+        int local[kSendPerThread];
+        int mine = 0;
 #pragma unroll
         for (int j = 0; j < kSendPerThread; ++j) {
-            const int q = i + j * kChunk;
-            if (q < g.R * g.R) sc_lds[q] = sc[j];
+            local[j] = mine;
+            mine += (i * kSendPerThread + j < nq) ? sc[j] : 0;
+        }
+        int all;
+        const int base = block_exclusive_scan(mine, wsum[0], &all);
+#pragma unroll
+        for (int j = 0; j < kSendPerThread; ++j) {
+            const int q = i * kSendPerThread + j;
+            if (q < nq) sc_lds[q] = base + local[j];
         }
         __syncthreads();
-        // send_offsets[s][d] = sum of send_counts[s][d'] over d' < d
 #pragma unroll
         for (int j = 0; j < kSendPerThread; ++j) {
-            const int q = i + j * kChunk;
-            if (q < g.R * g.R) {
-                const int s = q / g.R, d = q - s * g.R;
-                int run = 0;
-                for (int d2 = 0; d2 < d; ++d2) run += sc_lds[s * g.R + d2];
+            const int q = i * kSendPerThread + j;
+            if (q < nq) {
+                const int row0 = q - (q - small_quotient(q, g.R) * g.R);   // s * R
                 send_counts[q] = sc[j];
-                send_offsets[q] = run;
+                send_offsets[q] = base + local[j] - sc_lds[row0];
             }
         }
     }
@@ -378,7 +392,7 @@ __device__ __forceinline__ void layout_scatter_block(
             atomicOr(&bits[wave][g.E + __ffsll(static_cast<unsigned long long>(b)) - 1], me);
     }
     __syncthreads();
-    for (int col = threadIdx.x; col < g.W; col += blockDim.x) {
+    for (int col = threadIdx.x; col < g.W; col += kChunk) {
         int run = 0;
 #pragma unroll
         for (int w = 0; w < kWavesPerChunk; ++w) {
@@ -397,7 +411,7 @@ __device__ __forceinline__ void layout_scatter_block(
         if (P[s] >= 0) {
             const int Pe = P[s];
             sp = gbase[Pe] + pre[wave][Pe] + __popcll(bits[wave][Pe] & below);
-            const int d = Pe / g.E_loc;
+            const int d = small_quotient(Pe, g.E_loc);
             const int col = g.E + d;
             if ((m >> d) & 1ull) cr = gbase[col] + pre[wave][col] + __popcll(bits[wave][col] & below);
         }

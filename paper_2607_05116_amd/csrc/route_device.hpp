@@ -155,17 +155,6 @@ __device__ __forceinline__ constexpr uint64_t lanes_after_slot(int s) {
     return 0x0101010101010101ull * ((0xFFull << (s + 1)) & 0xFFull);
 }
 
-// floor(n / d) for 0 <= n < 2^31 and 1 <= d < 2^31 with a quotient below
-// 2^16: the fp32 estimate n * rcp(d) is within 2^-21 of n / d relative (so
-// within one of the quotient), and one correction step each way makes it exact.
-__device__ __forceinline__ int small_quotient(int n, int d) {
-    int q = static_cast<int>(static_cast<float>(n) * __builtin_amdgcn_rcpf(static_cast<float>(d)));
-    const long long r = static_cast<long long>(n) - static_cast<long long>(q) * d;
-    q += (r >= d) ? 1 : 0;
-    q -= (r < 0) ? 1 : 0;
-    return q;
-}
-
 constexpr int kDppMirror4 = 0x1B;       // quad_perm [3,2,1,0]
 
 // What a lane knows of its token after the decision: the expert of its slot
