@@ -51,13 +51,12 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     __shared__ int er_lds[kMaxE];
     __shared__ int pos_lds[kMaxE];
     __shared__ int hist[kRcWaves][kMaxW];
-    __shared__ int vsum[4];
+    __shared__ uint64_t vsum[kRcWaves];
     // expert tables in LDS, one entry per thread; their loads are issued
     // together with the logit loads (no branch, so no early wait)
     static_assert(kMaxE <= kRcThreads, "one table entry per thread");
     const int e_me = min(static_cast<int>(threadIdx.x), g.E - 1);
     const int er_v = expert_rank[e_me], el_v = expert_local[e_me];
-    if (threadIdx.x < 4) vsum[threadIdx.x] = 0;
     const int wave = threadIdx.x / kWave;
 #pragma unroll
     for (int w = 0; w < kRcWaves; ++w)
@@ -123,8 +122,10 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     if (col_e >= 0) atomicAdd(&hist[wave][col_e], 1);
     if (col_d >= 0) atomicAdd(&hist[wave][col_d], 1);
     // per-token volume (lane 0 of the token's group): n_dev, n_intra_remote,
-    // n_inter, n_nodes, and their sums over the part (integer LDS adds)
+    // n_inter, n_nodes, and their sums over the part (the four packed as
+    // 16-bit fields: a part's sums stay below 32 * 64 = 2^11)
     int v[4] = {0, 0, 0, 0};
+    uint64_t vp = 0;
     if (live && lg == 0) {
         // devices of one node: rpn consecutive bits; the source's node is `home`
         const uint64_t node_bits = (g.rpn >= 64) ? ~0ull : ((1ull << g.rpn) - 1);
@@ -138,18 +139,37 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
         }
         reinterpret_cast<uint32_t*>(vol)[t] = static_cast<uint32_t>(v[0]) | (static_cast<uint32_t>(v[1]) << 8) |
                                               (static_cast<uint32_t>(v[2]) << 16) | (static_cast<uint32_t>(v[3]) << 24);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) atomicAdd(&vsum[j], v[j]);
+        vp = static_cast<uint64_t>(v[0]) | (static_cast<uint64_t>(v[1]) << 16) |
+             (static_cast<uint64_t>(v[2]) << 32) | (static_cast<uint64_t>(v[3]) << 48);
     }
+    // the wave's 8 tokens (lanes 0, 8, ..., 56) summed by butterfly shuffles
+#pragma unroll
+    for (int off = kGroup; off < kWave; off <<= 1) {
+        const uint32_t lo = __shfl_xor(static_cast<uint32_t>(vp), off);
+        const uint32_t hi = __shfl_xor(static_cast<uint32_t>(vp >> 32), off);
+        vp += static_cast<uint64_t>(lo) | (static_cast<uint64_t>(hi) << 32);
+    }
+    if (lane_id() == 0) vsum[wave] = vp;
     __syncthreads();
-    if (threadIdx.x < 4) ws.volpart[sc * 4 + threadIdx.x] = vsum[threadIdx.x];
-    int32_t* out = ws.part + static_cast<size_t>(sc) * g.W;
-    for (int col = threadIdx.x; col < g.W; col += kRcThreads) {
-        int s = 0;
+    if (threadIdx.x < 4) {
+        uint64_t all = 0;
 #pragma unroll
-        for (int w = 0; w < kRcWaves; ++w) s += hist[w][col];
-        out[col] = s;
+        for (int w = 0; w < kRcWaves; ++w) all += vsum[w];
+        ws.volpart[sc * 4 + threadIdx.x] = static_cast<int64_t>((all >> (16 * threadIdx.x)) & 0xFFFFu);
     }
+    // the part's row: the waves' histograms summed (W <= 2 * 256: two
+    // columns per thread, the second clamped, all LDS reads issued together)
+    static_assert(kMaxW <= 2 * kRcThreads, "two columns per thread");
+    int32_t* out = ws.part + static_cast<size_t>(sc) * g.W;
+    const int col0 = threadIdx.x, col1 = min(static_cast<int>(threadIdx.x) + kRcThreads, g.W - 1);
+    int s0 = 0, s1 = 0;
+#pragma unroll
+    for (int w = 0; w < kRcWaves; ++w) {
+        s0 += hist[w][col0];
+        s1 += hist[w][col1];
+    }
+    if (col0 < g.W) out[col0] = s0;
+    if (col0 + kRcThreads < g.W) out[col1] = s1;
 }
 
 // Launch 2: blocks [0, W] scan the columns and sum the volumes; blocks
