@@ -10,9 +10,10 @@ namespace cap {
 namespace {
 
 
-constexpr int kThreads = 256;
-constexpr int kMaxSplitTokens = 512;   // <= 512 tokens x k^2 pairs stays below 2^16
-constexpr int kMaxSplits = 2048;
+constexpr int kThreads = 256;          // reduce blocks
+constexpr int kTileThreads = 256;      // tile blocks: one token per thread
+constexpr int kSplitTokens = 256;      // tokens per split (up to 512 keep k^2 x tokens below 2^16)
+static_assert(kSplitTokens == kTileThreads && kSplitTokens <= 512, "one token per tile thread");
 constexpr int kTriWordsMax = (kMaxE * (kMaxE + 1) / 2 + 1) / 2;
 constexpr int kTriQuadsMax = (kTriWordsMax + 3) / 4;
 constexpr int kReduceQuads = 32;                       // 16-byte columns per reduce block
@@ -35,25 +36,25 @@ __device__ __forceinline__ void coact_tile_block(int T, int k, int E, int tokens
     __shared__ uint4 tri4[kTriQuadsMax];
     uint32_t* tri = reinterpret_cast<uint32_t*>(tri4);
     const int TQ = tri_quads(E);
-    for (int i = threadIdx.x; i < TQ; i += kThreads) tri4[i] = make_uint4(0u, 0u, 0u, 0u);
+    for (int i = threadIdx.x; i < TQ; i += kTileThreads) tri4[i] = make_uint4(0u, 0u, 0u, 0u);
     __syncthreads();
     const int t_begin = bid * tokens_per_split;
     const int t_end = min(T, t_begin + tokens_per_split);
-    for (int t = t_begin + threadIdx.x; t < t_end; t += kThreads) {
+    for (int t = t_begin + threadIdx.x; t < t_end; t += kTileThreads) {
         int e[kMaxK];
         bool kp[kMaxK];
+        // every slot loaded unconditionally (slots past k reload slot k - 1 and
+        // are dropped below), so all the loads go out before the first wait
         const size_t q0 = static_cast<size_t>(t) * k;
 #pragma unroll
         for (int s = 0; s < kMaxK; ++s) {
-            e[s] = 0;
-            kp[s] = false;
-            if (s < k) {
-                e[s] = idx[q0 + s];
-                kp[s] = keep[q0 + s] != 0;
-            }
+            const size_t q = q0 + min(s, k - 1);
+            e[s] = idx[q];
+            kp[s] = keep[q] != 0;
         }
 #pragma unroll
-        for (int s = 0; s < kMaxK; ++s) kp[s] = kp[s] && static_cast<unsigned>(e[s]) < static_cast<unsigned>(E);
+        for (int s = 0; s < kMaxK; ++s)
+            kp[s] = kp[s] && s < k && static_cast<unsigned>(e[s]) < static_cast<unsigned>(E);
 #pragma unroll
         for (int a = 0; a < kMaxK; ++a) {
 #pragma unroll
@@ -72,16 +73,16 @@ __device__ __forceinline__ void coact_tile_block(int T, int k, int E, int tokens
     // (indices past the end are clamped to the last quad, which is then
     // written more than once with the same value: no branch, no early wait)
     uint4* out = reinterpret_cast<uint4*>(part) + static_cast<size_t>(bid) * TQ;
-    for (int i0 = threadIdx.x; i0 < TQ; i0 += 4 * kThreads) {
+    for (int i0 = threadIdx.x; i0 < TQ; i0 += 4 * kTileThreads) {
         uint4 v[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v[u] = tri4[min(i0 + u * kThreads, TQ - 1)];
+        for (int u = 0; u < 4; ++u) v[u] = tri4[min(i0 + u * kTileThreads, TQ - 1)];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) out[min(i0 + u * kThreads, TQ - 1)] = v[u];
+        for (int u = 0; u < 4; ++u) out[min(i0 + u * kTileThreads, TQ - 1)] = v[u];
     }
 }
 
-__global__ __launch_bounds__(kThreads) void coact_tile_kernel(
+__global__ __launch_bounds__(kTileThreads) void coact_tile_kernel(
     int T, int k, int E, int tokens_per_split, const int32_t* __restrict__ idx,
     const uint8_t* __restrict__ keep, uint32_t* __restrict__ part) {
     coact_tile_block(T, k, E, tokens_per_split, idx, keep, part, blockIdx.x);
@@ -153,11 +154,7 @@ __global__ __launch_bounds__(kThreads) void coact_reduce_kernel(
     coact_reduce_block(E, splits, accumulate, part, coact, blockIdx.x);
 }
 
-inline int coact_tokens_per_split(int T) {
-    int per = 256;
-    while (per < kMaxSplitTokens && (T + per - 1) / per > kMaxSplits) per *= 2;
-    return per;
-}
+inline int coact_tokens_per_split(int) { return kSplitTokens; }
 
 inline int coact_splits(int T) {
     const int per = coact_tokens_per_split(T);

@@ -31,7 +31,7 @@ cap_status coactivation_launch(int T, int k, int E, const int32_t* idx, const ui
     const int per = coact_tokens_per_split(T);
     const int S = coact_splits(T);
     uint32_t* part = static_cast<uint32_t*>(ws);
-    coact_tile_kernel<<<S, kThreads, 0, st>>>(T, k, E, per, idx, keep, part);
+    coact_tile_kernel<<<S, kTileThreads, 0, st>>>(T, k, E, per, idx, keep, part);
     CAP_LAUNCH_CHECK();
     coact_reduce_kernel<<<coact_reduce_blocks(E), kThreads, 0, st>>>(E, S, accumulate, part, coact);
     CAP_LAUNCH_CHECK();

@@ -40,7 +40,7 @@ constexpr int kParts = kChunk / kPart;                 // partial count rows per
 constexpr int kRcThreads = kPart * kGroup;             // 256
 constexpr int kRcWaves = kRcThreads / kWave;           // 4
 static_assert(kChunk % kPart == 0 && kRcThreads == 256, "one 8-lane group per token of a part");
-static_assert(kThreads == kChunk, "tile / reduce and scan / scatter blocks share one block size");
+static_assert(kThreads == kChunk, "co-activation reduce and scatter blocks share one block size");
 
 template <int V, int K, bool VEC>
 __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
@@ -172,15 +172,17 @@ __global__ __launch_bounds__(kRcThreads) void route_count_kernel(
     if (col0 + kRcThreads < g.W) out[col1] = s1;
 }
 
-// Launch 2: blocks [0, W] scan the columns and sum the volumes; blocks
-// [W + 1, W + 1 + splits) count the co-activation tiles.
-__global__ __launch_bounds__(kChunk) void front_scan_tile_kernel(Geom g, Workspace ws, int64_t* __restrict__ totals,
+// Launch 2 (blocks of kTileThreads): the first `splits` blocks count the
+// co-activation tiles (the longer work, so it starts first), the remaining
+// W + 1 scan the columns and sum the volumes.
+__global__ __launch_bounds__(kTileThreads) void front_scan_tile_kernel(Geom g, Workspace ws, int64_t* __restrict__ totals,
                                                                  const int32_t* __restrict__ idx,
                                                                  const uint8_t* __restrict__ keep, int per,
                                                                  uint32_t* __restrict__ coact_part) {
-    const int b = blockIdx.x;
-    if (b <= g.W) layout_colscan_block(g, ws, totals, b);
-    else coact_tile_block(g.T, g.k, g.E, per, idx, keep, coact_part, b - (g.W + 1));
+    const int splits = static_cast<int>(gridDim.x) - (g.W + 1);
+    const int b = static_cast<int>(blockIdx.x);
+    if (b < splits) coact_tile_block(g.T, g.k, g.E, per, idx, keep, coact_part, b);
+    else layout_colscan_block<kTileThreads>(g, ws, totals, b - splits);
 }
 
 // Launch 3: blocks [0, C) scatter the chunks; the rest reduce the
@@ -267,7 +269,7 @@ cap_status front_end_launch(const cap_topology* tp, const float* logits, float p
     CAP_LAUNCH_CHECK();
     const int per = coact_tokens_per_split(tp->T);
     const int splits = coact ? coact_splits(tp->T) : 0;
-    front_scan_tile_kernel<<<f.g.W + 1 + splits, kChunk, 0, st>>>(f.g, f.ws, o->totals, idx, keep, per,
+    front_scan_tile_kernel<<<f.g.W + 1 + splits, kTileThreads, 0, st>>>(f.g, f.ws, o->totals, idx, keep, per,
                                                                    f.coact_part);
     CAP_LAUNCH_CHECK();
     const int reduce_blocks = coact ? coact_reduce_blocks(tp->E) : 0;

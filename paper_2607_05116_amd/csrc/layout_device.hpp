@@ -57,20 +57,19 @@ __device__ __forceinline__ void load_token(const Geom& g, int t, const int32_t* 
                                            const int* pos_lds, int (&P)[kMaxK], uint64_t& m) {
     int e[kMaxK];
     uint8_t kp[kMaxK];
+    // every slot loaded unconditionally (slots past k reload slot k - 1 and are
+    // dropped below), so all the loads go out before the first wait
     const size_t q0 = static_cast<size_t>(t) * g.k;
 #pragma unroll
     for (int s = 0; s < kMaxK; ++s) {
-        e[s] = -1;
-        kp[s] = 0;
-        if (s < g.k) {
-            e[s] = idx[q0 + s];
-            kp[s] = keep[q0 + s];
-        }
+        const size_t q = q0 + min(s, g.k - 1);
+        e[s] = idx[q];
+        kp[s] = keep[q];
     }
     m = device_bits(mask[t], g.R);
 #pragma unroll
     for (int s = 0; s < kMaxK; ++s)
-        P[s] = (kp[s] && static_cast<unsigned>(e[s]) < static_cast<unsigned>(g.E)) ? pos_lds[e[s]] : -1;
+        P[s] = (kp[s] && s < g.k && static_cast<unsigned>(e[s]) < static_cast<unsigned>(g.E)) ? pos_lds[e[s]] : -1;
 }
 
 __device__ __forceinline__ int wave_sum(int v) {
@@ -80,6 +79,7 @@ __device__ __forceinline__ int wave_sum(int v) {
 }
 
 // Exclusive scan over the 256 threads of a block; *total gets the sum.
+template <int NW = kWavesPerChunk>
 __device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* total) {
     const int lane = lane_id(), wave = threadIdx.x / kWave;
     int inc = v;
@@ -92,7 +92,7 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* total
     __syncthreads();
     int before = 0, all = 0;
 #pragma unroll
-    for (int w = 0; w < kWavesPerChunk; ++w) {
+    for (int w = 0; w < NW; ++w) {
         if (w < wave) before += wsum[w];
         all += wsum[w];
     }
@@ -159,15 +159,20 @@ __global__ __launch_bounds__(kChunk) void layout_count_kernel(
 // ---------------------------------------------------------------- 2. colscan
 constexpr int kScanBatch = 8;
 
-// Column scan, block bid of g.W + 1: one block per column scans it over the
-// Cs partial rows (in place: counts -> exclusive bases) and writes its total;
-// block g.W sums the volumes.
+// Column scan, block bid of g.W + 1: one block of NT threads per column scans
+// it over the Cs partial rows (in place: counts -> exclusive bases) and writes
+// its total; block g.W sums the volumes.  When a thread's rows fit one batch
+// (Cs <= 8 NT) they are read once, clamped rather than tested, so the block
+// waits for one round of loads.
+template <int NT>
 __device__ __forceinline__ void layout_colscan_block(const Geom& g, const Workspace& ws, int64_t* __restrict__ totals,
                                                      int bid) {
-    __shared__ int wsum[kWavesPerChunk];
+    constexpr int NW = NT / kWave;
+    __shared__ int wsum[NW];
     if (bid == g.W) {
-        // volume totals: wave j sums column j of volpart
+        // volume totals: wave j < 4 sums column j of volpart
         const int j = threadIdx.x / kWave;
+        if (j >= 4) return;
         int64_t s = 0;
         for (int c = lane_id(); c < g.Cs; c += kWave) s += ws.volpart[c * 4 + j];
 #pragma unroll
@@ -176,34 +181,54 @@ __device__ __forceinline__ void layout_colscan_block(const Geom& g, const Worksp
         return;
     }
     const int col = bid;
-    const int per = (g.Cs + kChunk - 1) / kChunk;         // partial rows per thread, consecutive
+    const int per = (g.Cs + NT - 1) / NT;                 // partial rows per thread, consecutive
     const int c0 = min(g.Cs, static_cast<int>(threadIdx.x) * per);
     const int c1 = min(g.Cs, c0 + per);
-    int mine = 0;
-    for (int b = c0; b < c1; b += kScanBatch) {
-        int x[kScanBatch];
-#pragma unroll
-        for (int i = 0; i < kScanBatch; ++i) x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
-#pragma unroll
-        for (int i = 0; i < kScanBatch; ++i) mine += x[i];
-    }
     int total;
-    int run = block_exclusive_scan(mine, wsum, &total);
-    for (int b = c0; b < c1; b += kScanBatch) {
+    if (per <= kScanBatch) {
         int x[kScanBatch];
-#pragma unroll
-        for (int i = 0; i < kScanBatch; ++i) x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
 #pragma unroll
         for (int i = 0; i < kScanBatch; ++i) {
-            if (b + i < c1) ws.part[static_cast<size_t>(b + i) * g.W + col] = run;
+            x[i] = ws.part[static_cast<size_t>(min(c0 + i, g.Cs - 1)) * g.W + col];
+            if (c0 + i >= c1) x[i] = 0;
+        }
+        int mine = 0;
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) mine += x[i];
+        int run = block_exclusive_scan<NW>(mine, wsum, &total);
+#pragma unroll
+        for (int i = 0; i < kScanBatch; ++i) {
+            if (c0 + i < c1) ws.part[static_cast<size_t>(c0 + i) * g.W + col] = run;
             run += x[i];
+        }
+    } else {
+        int mine = 0;
+        for (int b = c0; b < c1; b += kScanBatch) {
+            int x[kScanBatch];
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i)
+                x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) mine += x[i];
+        }
+        int run = block_exclusive_scan<NW>(mine, wsum, &total);
+        for (int b = c0; b < c1; b += kScanBatch) {
+            int x[kScanBatch];
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i)
+                x[i] = (b + i < c1) ? ws.part[static_cast<size_t>(b + i) * g.W + col] : 0;
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) {
+                if (b + i < c1) ws.part[static_cast<size_t>(b + i) * g.W + col] = run;
+                run += x[i];
+            }
         }
     }
     if (threadIdx.x == 0) ws.coltot[col] = total;
 }
 
 __global__ __launch_bounds__(kChunk) void layout_colscan_kernel(Geom g, Workspace ws, int64_t* __restrict__ totals) {
-    layout_colscan_block(g, ws, totals, blockIdx.x);
+    layout_colscan_block<kChunk>(g, ws, totals, blockIdx.x);
 }
 
 // ---------------------------------------------------------------- 3. scatter
