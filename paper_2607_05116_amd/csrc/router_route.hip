@@ -8,7 +8,9 @@
 // GEMM: logits[t][e] = sum_k x[t][k] * W_g[e][k], bf16 operands, fp32
 // accumulation in K order per 16-wide MFMA step.  K = d in stages of 64
 // (one 128-byte line per operand row) filled by direct-to-LDS loads into a
-// double buffer.  A block holds BT = 128 or 64 tokens; each of its four waves
+// ring of three buffers, two stages in flight.  A block holds BT = 128 or 64
+// tokens (128 when E > 128, halving the router-weight reads, which then
+// dominate the loads); each of its four waves
 // owns 32 tokens and all (BT = 128) or half (BT = 64) of the expert columns
 // (v_mfma_f32_32x32x16_bf16 with the W_g fragment first, so a lane holds one
 // token's logits for 16 experts per 32-expert block).  The expert dimension is
@@ -20,6 +22,7 @@ namespace cap {
 namespace {
 
 constexpr int kRtK = 64;           // K per stage
+constexpr int kRtStages = 3;       // stage buffers in LDS (two stages in flight)
 constexpr int kRtRowB = kRtK * 2;  // bytes per LDS row (one 128-byte line)
 
 typedef __attribute__((address_space(3))) void rt_lds_void;
@@ -57,11 +60,12 @@ __global__ __launch_bounds__(256) void router_route_kernel(
     constexpr int STAGE_B = NR * kRtRowB;
     constexpr int LPITCH = EP + 4;                          // logits row pitch (floats), padded
     constexpr int TILE_B = BT * LPITCH * 4;
-    constexpr int LDS_B = 2 * STAGE_B > TILE_B ? 2 * STAGE_B : TILE_B;
+    constexpr int LDS_B = kRtStages * STAGE_B > TILE_B ? kRtStages * STAGE_B : TILE_B;
     constexpr int WE = 4 / (BT / 32);                       // waves sharing a 32-token group
     constexpr int NJ = EP / 32 / WE;                        // 32-expert MFMA blocks per wave
     constexpr int LOADS = NR / 8;                           // 1 KB direct loads per stage
     constexpr int LOADS_PER_WAVE = (LOADS + 3) / 4;
+    constexpr int LOADS_MIN_WAVE = LOADS / 4;               // loads of a stage every wave has issued
     static_assert(BT == 64 || BT == 128, "four waves of 32 tokens, or two per token group");
     static_assert(EP % 32 == 0 && EP >= 8 * V && (EP / 32) % WE == 0, "padded expert columns");
     static_assert(LDS_B + kMaxE * 4 <= 160 * 1024, "LDS");
@@ -85,7 +89,7 @@ __global__ __launch_bounds__(256) void router_route_kernel(
 #pragma unroll
         for (int ii = 0; ii < LOADS_PER_WAVE; ++ii) {
             const int i = ii * 4 + wave;
-            if (i >= LOADS) break;                          // wave-uniform
+            if (LOADS % 4 != 0 && i >= LOADS) break;        // wave-uniform
             const int r = 8 * i + (lane >> 3);
             const int chunk = (lane & 7) ^ rt_swz(r);
             const char* row = (i < BT / 8)
@@ -106,23 +110,51 @@ __global__ __launch_bounds__(256) void router_route_kernel(
     const int fr_row = lane & 31;
     const int fr_swz = rt_swz(fr_row);          // = rt_swz of the fragment's stage row
     const int fr_half = lane >> 5;
-    issue_stage(0, 0);
-    for (int kt = 0; kt < KT; ++kt) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's loads of stage kt landed
-        rt_barrier();                                        // stage kt complete; the other buffer is free
-        if (kt + 1 < KT) issue_stage(kt + 1, (kt + 1) & 1);
-        const uint8_t* sx = lds + (kt & 1) * STAGE_B;        // token rows
+    // Ring of kRtStages buffers, two stages in flight, and the fragments one
+    // K step ahead of the MFMAs.  A stage's last K step reads its fragments,
+    // then the wave waits until only the loads of the stage after next (at
+    // least LOADS_MIN_WAVE of its own) can still be pending, so the next stage
+    // has landed; after the barrier every wave is done reading the current
+    // stage, whose buffer takes the stage three ahead, and the next stage's
+    // first fragments are read while the current MFMAs run.
+    constexpr int KS = kRtK / 16;                            // K steps per stage
+    static_assert(KS % 2 == 0, "the fragment sets alternate within a stage");
+    auto read_frags = [&](int stage_buf, int ks, bf16x8& fx, bf16x8 (&fw)[NJ]) {
+        const uint8_t* sx = lds + stage_buf * STAGE_B;       // token rows
         const uint8_t* sw = sx + BT * kRtRowB + we * NJ * 32 * kRtRowB;   // this wave's expert rows
+        const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
+        fx = *reinterpret_cast<const bf16x8*>(sx + (wt * 32 + fr_row) * kRtRowB + pc);
 #pragma unroll
-        for (int ks = 0; ks < kRtK / 16; ++ks) {
-            const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
-            const bf16x8 fx = *reinterpret_cast<const bf16x8*>(sx + (wt * 32 + fr_row) * kRtRowB + pc);
+        for (int j = 0; j < NJ; ++j) fw[j] = *reinterpret_cast<const bf16x8*>(sw + (j * 32 + fr_row) * kRtRowB + pc);
+    };
+    issue_stage(0, 0);
+    if (KT > 1) issue_stage(1, 1);
+    if (KT > 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS_MIN_WAVE) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    rt_barrier();                                            // stage 0 complete in every wave
+    if (KT > 2) issue_stage(2, 2);
+    bf16x8 fx[2], fw[2][NJ];
+    read_frags(0, 0, fx[0], fw[0]);
+    int buf = 0;                                             // buffer of stage kt
+    for (int kt = 0; kt < KT; ++kt) {
+        const int nbuf = (buf + 1 == kRtStages) ? 0 : buf + 1;
 #pragma unroll
-            for (int j = 0; j < NJ; ++j) {
-                const bf16x8 fw = *reinterpret_cast<const bf16x8*>(sw + (j * 32 + fr_row) * kRtRowB + pc);
-                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw, fx, acc[j], 0, 0, 0);
+        for (int ks = 0; ks < KS; ++ks) {
+            const int cur = ks & 1, nxt = cur ^ 1;
+            if (ks + 1 < KS) {
+                read_frags(buf, ks + 1, fx[nxt], fw[nxt]);
+            } else if (kt + 1 < KT) {
+                if (kt + 2 < KT) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS_MIN_WAVE) : "memory");
+                else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                rt_barrier();                                // stage kt + 1 complete; stage kt read by all
+                if (kt + 3 < KT) issue_stage(kt + 3, buf);
+                read_frags(nbuf, 0, fx[nxt], fw[nxt]);
             }
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fw[cur][j], fx[cur], acc[j], 0, 0, 0);
         }
+        buf = nbuf;
     }
 
     // Logits tile [BT][EP] in LDS over the stage buffers: lane l holds token
@@ -180,7 +212,9 @@ template <int V, int K>
 void launch_router_route(const cap_topology* tp, int d, const uint16_t* x, const uint16_t* wg, float p,
                          int32_t* idx, float* w, uint8_t* keep, uint64_t* mask, float* logits, hipStream_t st) {
     constexpr int EP = 8 * V > 32 ? 8 * V : 32;
-    constexpr int BT = EP >= 64 ? 64 : 128;      // 64-token blocks when the experts split in two
+    // 128-token blocks halve the router-weight reads per token where they
+    // dominate (E > 128); with fewer experts 64-token blocks give more blocks
+    constexpr int BT = (EP > 128 || EP < 64) ? 128 : 64;
     const int blocks = (tp->T + BT - 1) / BT;
     if (tp->E == 8 * V)
         router_route_kernel<V, K, EP, BT, true><<<blocks, 256, 0, st>>>(
