@@ -14,11 +14,12 @@
 //                      Each wave adds its tokens' counts into a histogram of
 //                      its own with integer LDS adds (exact, so the counts do
 //                      not depend on the order they land in), and the 4 wave
-//                      histograms are summed in a fixed order; no global
-//                      atomics.
-//   2. scan + tiles    the column scans over the part rows (exclusive
-//                      bases in place) and the volume totals, beside the
-//                      co-activation tile blocks (one per split of tokens).
+//                      histograms are summed in a fixed order; the volume
+//                      sums go through wave shuffles; no global atomics.
+//   2. tiles + scan    the co-activation tile blocks (one per split of
+//                      tokens, dispatched first: the longer work), beside
+//                      the column scans over the part rows (exclusive bases
+//                      in place) and the volume totals.
 //   3. scatter + sum   the stable scatter of each 256-token chunk (its base is
 //                      the scanned row of its first part), beside the
 //                      co-activation reduce blocks.
