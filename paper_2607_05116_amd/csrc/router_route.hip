@@ -146,6 +146,9 @@ __global__ __launch_bounds__(256) void router_route_kernel(
             } else if (kt + 1 < KT) {
                 if (kt + 2 < KT) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(LOADS_MIN_WAVE) : "memory");
                 else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                // this wave's reads of stage kt have returned before its buffer
+                // can be handed to the loads of stage kt + 3
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
                 rt_barrier();                                // stage kt + 1 complete; stage kt read by all
                 if (kt + 3 < KT) issue_stage(kt + 3, buf);
                 read_frags(nbuf, 0, fx[nxt], fw[nxt]);
