@@ -36,7 +36,9 @@
 // candidate devices (one lane each) are sorted across the group with the same
 // kind of packed-double keys; every lane replays the greedy's running sum over
 // the ranked list, which fixes how many of the ranked devices are kept, and
-// the group ORs the kept devices' bits into the mask.
+// the group ORs the kept devices' bits into the mask.  Rows of 64, 128 or 256
+// logits take the four-lane form below (route_prune4_kernel), which computes
+// the same bits with all of a token's cross-lane traffic inside one quad.
 #pragma clang fp contract(off)
 
 #include <math.h>
