@@ -317,10 +317,15 @@ def _adversarial_logits(T, E, seed):
     return L
 
 
-@pytest.mark.parametrize("E,k,R,rpn,p,c", [
+ADV_SHAPES = [
     (16, 2, 4, 4, 0.3, 5.0), (64, 6, 8, 4, 0.25, 5.0), (128, 8, 16, 8, 0.1, 5.0),
     (256, 8, 32, 8, 0.2, 3.0), (7, 3, 1, 1, 0.4, 5.0), (24, 5, 6, 2, 0.5, 2.0),
-    (128, 8, 64, 8, 0.3, 5.0), (96, 1, 8, 8, 0.0, 5.0), (40, 8, 4, 2, 0.05, 5.0)])
+    (128, 8, 64, 8, 0.3, 5.0), (96, 1, 8, 8, 0.0, 5.0), (40, 8, 4, 2, 0.05, 5.0),
+    # the four-lane kernel with one slot per lane (k <= 4) and a partly filled second slot
+    (64, 4, 8, 4, 0.2, 5.0), (256, 3, 16, 8, 0.3, 3.0), (128, 1, 8, 8, 0.1, 5.0), (128, 5, 16, 4, 0.25, 5.0)]
+
+
+@pytest.mark.parametrize("E,k,R,rpn,p,c", ADV_SHAPES)
 def test_route_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
     T = R * 160
     L = _adversarial_logits(T, E, E + k)
@@ -339,6 +344,29 @@ def test_route_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
     for name in ("slot_pos", "copy_row", "vol", "expert_offsets", "send_counts", "totals"):
         assert np.array_equal(Ld.host(name), lay[name]), name
     assert np.array_equal(Ld.host("coact").view(np.uint32), oracle.coactivation(r["idx"], r["keep"], E))
+
+
+@pytest.mark.parametrize("E,k,R,rpn,p,c", ADV_SHAPES)
+def test_route_naive_adversarial_and_odd_shapes(E, k, R, rpn, p, c):
+    """Expert-level pruning (cap_route_prune_naive) on the adversarial logits
+    and shapes, against the oracle's top-k, gates and naive pruning."""
+    T = R * 160
+    L = _adversarial_logits(T, E, E + k + 1)
+    perm = np.random.default_rng(R + 1).permutation(E)
+    er, el = (perm // (E // R)).astype(np.int32), (perm % (E // R)).astype(np.int32)
+    cfg = gen.Config("adv", T=T, d=8, E=E, k=k, inter=128, R=R, ranks_per_node=rpn, n_clusters=1,
+                     zipf_s=0.0, dtype="bf16")
+    Ld = DeviceLayer(cfg, L, np.zeros((T, 8), np.uint16), er, el, p, c, row_cap=8, recv_cap=8)
+    Ld.naive = True
+    Ld.route()
+    torch.cuda.synchronize()
+    idx = oracle.topk(L, k)
+    w = oracle.gates(L, idx)
+    keep, wp, mask = oracle.prune_naive(idx, w, er, p)
+    assert np.array_equal(Ld.host("idx"), idx)
+    assert np.array_equal(Ld.host("w").view(np.uint32), wp.view(np.uint32))
+    assert np.array_equal(Ld.host("keep"), keep)
+    assert np.array_equal(Ld.host("mask").view(np.uint64), mask)
 
 
 def _edge_logits(T, E, k, seed):
