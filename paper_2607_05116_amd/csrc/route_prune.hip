@@ -374,14 +374,17 @@ void launch_route_mode(const cap_topology* tp, const float* logits, float p, int
         }
     }
     const int blocks = (tp->T + kTokensPerBlock - 1) / kTokensPerBlock;
-    if (vec_ok)
-        route_prune_kernel<V, K, true, NAIVE><<<blocks, 256, 0, st>>>(
-            logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
-            tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
-    else
-        route_prune_kernel<V, K, false, NAIVE><<<blocks, 256, 0, st>>>(
-            logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
-            tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
+    if constexpr (V < 8) {                      // the vector-load eight-lane form only where no quad form exists
+        if (vec_ok) {
+            route_prune_kernel<V, K, true, NAIVE><<<blocks, 256, 0, st>>>(
+                logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
+                tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
+            return;
+        }
+    }
+    route_prune_kernel<V, K, false, NAIVE><<<blocks, 256, 0, st>>>(
+        logits, tp->T, tp->E, tp->R, tp->ranks_per_node, tp->tokens_per_rank,
+        tp->inter_node_cost, p, tp->expert_rank, idx, w, keep, mask);
 }
 
 template <int V, int K>
