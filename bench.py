@@ -65,6 +65,9 @@ def parse():
     ap.add_argument("--aux-config", default="c2",
                     help="second workload measured briefly into aux (graph-replayed step and FFN); "
                          "'none' to skip")
+    ap.add_argument("--vendor", action="store_true",
+                    help="also time the vendor library (torch.matmul, hipBLASLt) on the same rank's grouped "
+                         "SwiGLU FFN, one GEMM pair per expert, into aux.vendor_grouped_ffn (for comparison)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run 3 device-to-device copies of MIB MiB (HBM counter calibration) and exit")
     return ap.parse_args()
@@ -570,6 +573,9 @@ def main():
     }
     if not args.quick:
         result["aux"].update(detail_measurements(args, L, cfg, rank, stream, totals))
+    if args.vendor:
+        log("vendor library on the same grouped FFN ...")
+        result["aux"]["vendor_grouped_ffn"] = vendor_grouped_ffn(L, cfg, rank, flops)
     if not args.no_cpu:
         log("timing the CPU oracle on a bounded sample ...")
         result["cpu_baseline"] = cpu_baseline(cfg, args.p, args.c, logits, x, args.cpu_stride)
@@ -580,6 +586,57 @@ def main():
         log(f"second workload {args.aux_config} ...")
         result["aux"]["second_workload"] = aux_workload(args.aux_config, rank, K, args.warmup, args.c)
     print(json.dumps(result), flush=True)
+
+
+def vendor_grouped_ffn(L, cfg, rank, flops, reps=20, warmup=30):
+    """The vendor library on the rank's FFN: for each local expert, torch.matmul
+    (hipBLASLt) of its gathered rows with [W1; W3] (one GEMM), SiLU(gate) * up,
+    and the down GEMM with W2, on the same rows and weights as the fused call;
+    timed with HIP events after a warmup long enough for the clock to settle.
+    For comparison only: the product path never calls it."""
+    import torch
+    E_loc = cfg.E_loc
+    eo = L.host("expert_offsets")[rank * E_loc:(rank + 1) * E_loc + 1].astype("int64")
+    rows = int(eo[-1] - eo[0])
+    L.row_source(rank)
+    xs = L.x.index_select(0, L.row_src[:rows].long())
+    w1, w3, w2 = L.weights[rank]
+    w13 = [torch.cat([w1[l], w3[l]], 0).contiguous() for l in range(E_loc)]
+    w2c = [w2[l].contiguous() for l in range(E_loc)]
+    inter = cfg.inter
+    spans = [(int(eo[l] - eo[0]), int(eo[l + 1] - eo[0])) for l in range(E_loc)]
+
+    def ffn():
+        for l, (a, b) in enumerate(spans):
+            if b > a:
+                h = torch.matmul(xs[a:b], w13[l].t())
+                torch.matmul(torch.nn.functional.silu(h[:, :inter]) * h[:, inter:], w2c[l].t())
+
+    def gemms_only():
+        for l, (a, b) in enumerate(spans):
+            if b > a:
+                h = torch.matmul(xs[a:b], w13[l].t())
+                torch.matmul(h[:, :inter], w2c[l].t())
+
+    out = {"library": "torch.matmul (hipBLASLt), one [W1; W3] GEMM and one W2 GEMM per expert",
+           "experts": E_loc, "rows": rows}
+    for fn, key in ((ffn, "swiglu"), (gemms_only, "gemms_only")):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        out[f"{key}_ms"] = ms
+        out[f"{key}_tflops"] = flops / (ms * 1e-3) / 1e12
+        out[f"{key}_frac_bf16_peak"] = flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS
+    del xs, w13, w2c
+    torch.cuda.empty_cache()
+    return out
 
 
 def detail_measurements(args, L, cfg, rank, stream, totals):

@@ -6,7 +6,7 @@
 //   gate/up   H[m][j] = silu(X W1^T)[m][j] * (X W3^T)[m][j]   (K = d)
 //   down      Y[m][o] = (H W2^T)[m][o]                         (K = inter)
 //
-// bf16 path (gfx950 MFMA v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+// bf16 path (gfx950 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation):
 //   * Block tile 256 x 256, eight waves (two per SIMD) of 64 x 128 each.
 //   * Operands are both K-contiguous (token rows of X / H; weight rows of W).
 //     gfx950 direct-to-LDS loads (global_load_lds_dwordx4) fill a double
@@ -16,7 +16,9 @@
 //   * Half of the waves issue all the stage loads and the other half all the
 //     output stores, so no wave's in-order memory counter mixes the two (a
 //     wait for a stage never waits for a tile's worth of stores to drain).
-//   * Each wave reads its LDS fragments one MFMA K step ahead of its MFMAs.
+//   * Each wave reads its LDS fragments one MFMA K step ahead of its MFMAs
+//     (16 x 16 x 32 MFMAs: half the accumulator reads and writes per flop of
+//     the 32 x 32 x 16 form, measured 3-4 % faster on whole calls).
 //   * Calls of many m-tiles run both GEMMs in one persistent kernel with a
 //     tile queue per XCD (ffn_fused_bf16_kernel); calls of few m-tiles run one
 //     persistent kernel per GEMM (ffn_gemm_bf16_kernel).  Every output element
@@ -189,7 +191,7 @@ constexpr int kBM = 256, kBN = 256, kWavesM = 4, kWavesN = 2;
 constexpr int kNW = kWavesM * kWavesN;
 constexpr int kNL = kNW / 2;                          // loader waves; the rest are storers
 constexpr int kWM = kBM / kWavesM, kWN = kBN / kWavesN;
-constexpr int kMI = kWM / 32, kNJ = kWN / 32;         // 32 x 32 MFMA blocks per wave
+constexpr int kMI = kWM / 16, kNJ = kWN / 16;         // 16 x 16 MFMA blocks per wave
 constexpr int kRowsPerLoad = 1024 / kRowB;            // rows one wave-wide 16-byte load covers
 constexpr int kALd = kBM / kRowsPerLoad / kNL;        // direct loads per loader wave per stage
 constexpr int kBLd = kBN / kRowsPerLoad / kNL;
@@ -201,7 +203,8 @@ static_assert(kALd + kBLd <= 60, "loads per stage must fit the vmcnt field");
 static_assert(kWN % 64 == 0, "gate/up pairs need 64-column wave tiles");
 static_assert(kBRun * kRowsPerLoad == 32, "a gate/up loader covers one 32-row W1/W3 pair");
 static_assert(kALd * kRowsPerLoad == kWM, "loader wave w loads the A rows that waves of row w read");
-static_assert(kStageK % 32 == 0, "fragments are read two K steps at a time");
+static_assert(kStageK == 64, "a stage is two MFMA K steps of 32");
+static_assert(kNJ >= kMI, "the next step's A fragments are read after the first kMI B blocks");
 static_assert(kStages == 2, "staging lives in stage buffer 1");
 
 // Per-lane constants of the direct loads and the fragment reads.
@@ -209,7 +212,7 @@ struct LaneMap {
     int ld_row;          // direct loads: lane l writes row l / 8 of its 1 KiB block ...
     uint32_t col_b[2];   // ... at physical chunk l % 8, fetching logical chunk (l % 8) ^ swz(row):
                          // the swizzle of row (8 * blk + l / 8) is swz(l / 8) ^ (blk & 1)
-    int fr_row, fr_swz, fr_half;   // fragment reads: row r = ... + lane % 32, K half lane / 32
+    int fr_row, fr_swz, fr_q;      // fragment reads: row r = ... + lane % 16, K quarter lane / 16
 };
 __device__ __forceinline__ LaneMap lane_map(int lane) {
     LaneMap m;
@@ -217,85 +220,78 @@ __device__ __forceinline__ LaneMap lane_map(int lane) {
     const int pc = lane & (kChunks - 1);
     m.col_b[0] = static_cast<uint32_t>((pc ^ lds_swz(m.ld_row)) * 16);
     m.col_b[1] = static_cast<uint32_t>((pc ^ lds_swz(kRowsPerLoad + m.ld_row)) * 16);
-    m.fr_row = lane & 31;
+    m.fr_row = lane & 15;
     m.fr_swz = lds_swz(m.fr_row);
-    m.fr_half = lane >> 5;
+    m.fr_q = lane >> 4;
     return m;
 }
 
-// Fragments of one MFMA K step (K = 16) of a wave's 64 x 128 block: kMI A
-// fragments and kNJ B fragments, one 16-byte LDS read each.  Lane (r, h) =
-// (lane % 32, lane / 32) reads row r of each 32-row block, K half h.
-struct Frags {
-    bf16x8 a[kMI], b[kNJ];
-};
+// Fragments and MFMAs.  One MFMA K step is K = 32 (two per stage).  Lane
+// (r, q) = (lane % 16, lane / 16) reads row r of each 16-row block at 16-byte
+// chunk 4 ks + q of K step ks (8 consecutive K; A and B take the same K
+// positions, so the contraction pairs them correctly whatever order the
+// hardware sums them in).  The MFMA takes the weight fragment as its first
+// operand, so a lane's 4 accumulators of block (i, j) hold output columns
+// 16 j + 4 q + 0..3 of tile row 16 i + r.
+__device__ __forceinline__ const bf16x8& frag_at(const uint8_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
-__device__ __forceinline__ void read_frags(const uint8_t* st, int ks, int wm, int wn, int fr_row, int fr_swz,
-                                           int fr_half, Frags& f) {
-    const int pc = ((2 * ks + fr_half) ^ fr_swz) << 4;
-    const uint8_t* sb = st + kBM * kRowB;
+// One K step of a wave's 64 x 128 block: its kMI x kNJ MFMAs, B block outer.
+// With rd, the fragments of the next K step (K step nks of the stage at nst)
+// are read between them: B fragment j into b[j] right after the last MFMA
+// that uses it, and the A fragments into the other set an (after the first
+// kMI B blocks), so one step's MFMAs cover the next step's LDS latency with
+// 64 fragment registers per lane.
+__device__ __forceinline__ void k_step(const bf16x8 (&ac)[kMI], bf16x8 (&an)[kMI], bf16x8 (&b)[kNJ],
+                                       f32x4 (&acc)[kMI][kNJ], const uint8_t* nst, int nks, int wm, int wn,
+                                       const LaneMap& lm, bool rd) {
+    const int pc = ((4 * nks + lm.fr_q) ^ lm.fr_swz) << 4;
+    const uint8_t* sa = nst + (wm * kWM + lm.fr_row) * kRowB + pc;
+    const uint8_t* sb = nst + (kBM + wn * kWN + lm.fr_row) * kRowB + pc;
 #pragma unroll
-    for (int i = 0; i < kMI; ++i)
-        f.a[i] = *reinterpret_cast<const bf16x8*>(st + (wm * kWM + i * 32 + fr_row) * kRowB + pc);
+    for (int j = 0; j < kNJ; ++j) {
 #pragma unroll
-    for (int j = 0; j < kNJ; ++j)
-        f.b[j] = *reinterpret_cast<const bf16x8*>(sb + (wn * kWN + j * 32 + fr_row) * kRowB + pc);
-}
-
-// The MFMAs of one K step.  The MFMA takes the weight fragment as its first
-// operand, so a lane's 16 accumulators hold 4 consecutive output columns per
-// register group.
-__device__ __forceinline__ void mma_frags(const Frags& f, f32x16 (&acc)[kMI][kNJ]) {
-#pragma unroll
-    for (int i = 0; i < kMI; ++i)
-#pragma unroll
-        for (int j = 0; j < kNJ; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.b[j], f.a[i], acc[i][j], 0, 0, 0);
-}
-
-// The MFMAs of the current K step with the fragment reads of the next one
-// (K step ks of the stage at st) issued between them, so that the LDS latency
-// of the next step hides behind this step's MFMAs.
-__device__ __forceinline__ void mma_and_read(const Frags& cur, f32x16 (&acc)[kMI][kNJ], const uint8_t* st, int ks,
-                                             int wm, int wn, int fr_row, int fr_swz, int fr_half, Frags& nxt) {
-    read_frags(st, ks, wm, wn, fr_row, fr_swz, fr_half, nxt);
-    mma_frags(cur, acc);
-    static_for<kMI + kNJ>([&](auto) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one DS read
+        for (int i = 0; i < kMI; ++i)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(b[j], ac[i], acc[i][j], 0, 0, 0);
+        if (rd) {
+            if (j < kMI) an[j] = frag_at(sa + j * 16 * kRowB);
+            b[j] = frag_at(sb + j * 16 * kRowB);
+        }
+    }
+    static_for<kNJ>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        __builtin_amdgcn_sched_group_barrier(0x008, kMI, 0);                 // block j's MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x100, j < kMI ? 2 : 1, 0);     // its fragment reads
     });
-    __builtin_amdgcn_sched_group_barrier(0x008, kMI * kNJ - (kMI + kNJ), 0);
 }
 
-// The K loop of one tile: KT stages of K = 64 (four K steps each).
+// The K loop of one tile: KT stages of K = 64 (two K steps each).
 // sync(kt) makes stage kt visible and issues the loads of stage kt + 1 (the
 // loaders' wait for their own loads, the workgroup barrier, the next issue and
 // any per-stage bookkeeping of the caller).  A wave's fragment reads run one K
 // step ahead of its MFMAs; the barrier of stage kt + 1 comes after the reads of
-// stage kt's last K step have returned (so the loads issued after it may
+// stage kt's second K step have returned (so the loads issued after it may
 // overwrite stage kt's buffer) and before that step's MFMAs.  A wave whose
 // 64 rows all lie past the tile's valid rows (active = false) computes
 // nothing: its accumulators stay zero and are never stored.
 template <typename Sync>
 __device__ __forceinline__ void k_loop(int KT, const uint8_t* lds, int wm, int wn, const LaneMap& lm, bool active,
-                                       f32x16 (&acc)[kMI][kNJ], Sync&& sync) {
-    Frags f0, f1;
+                                       f32x4 (&acc)[kMI][kNJ], Sync&& sync) {
+    bf16x8 a0[kMI], a1[kMI], b[kNJ];
     sync(0);
-    if (active) read_frags(lds, 0, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f0);
+    if (active) {
+        const int pc = (lm.fr_q ^ lm.fr_swz) << 4;
+#pragma unroll
+        for (int i = 0; i < kMI; ++i) a0[i] = frag_at(lds + (wm * kWM + i * 16 + lm.fr_row) * kRowB + pc);
+#pragma unroll
+        for (int j = 0; j < kNJ; ++j) b[j] = frag_at(lds + (kBM + wn * kWN + j * 16 + lm.fr_row) * kRowB + pc);
+    }
     for (int kt = 0; kt < KT; ++kt) {
-        const uint8_t* st = lds + (kt % kStages) * kStageBytes;
-        if (active) {
-            mma_and_read(f0, acc, st, 1, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f1);
-            mma_and_read(f1, acc, st, 2, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f0);
-            mma_and_read(f0, acc, st, 3, wm, wn, lm.fr_row, lm.fr_swz, lm.fr_half, f1);
-        }
+        if (active) k_step(a0, a1, b, acc, lds + (kt % kStages) * kStageBytes, 1, wm, wn, lm, true);
         asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");       // stage kt fully read
         // stage kt + 1 visible (after the last stage: a plain barrier; the
         // fragments read after it are never used)
         sync(kt + 1);
-        if (active)
-            mma_and_read(f1, acc, lds + ((kt + 1) % kStages) * kStageBytes, 0, wm, wn, lm.fr_row, lm.fr_swz,
-                         lm.fr_half, f0);
+        if (active) k_step(a1, a0, b, acc, lds + ((kt + 1) % kStages) * kStageBytes, 0, wm, wn, lm, true);
     }
 }
 
@@ -327,14 +323,15 @@ __device__ __forceinline__ u32x4 scale_chunk(const u32x4& v, float w) {
 }
 
 // Epilogue of a tile of rows [row0, row0 + rows) and block column nt.
-// Lane (r, h) = (lane % 32, lane / 32) holds, for register group g, columns
-// 8g + 4h + 0..3 of row r of each 32 x 32 block.  Lanes r and r + 32 swap
-// halves (permlane32_swap) so that each holds 8 consecutive columns: groups
-// (0, 1) -> lane r columns 0..7, lane r + 32 columns 8..15; groups (2, 3)
-// likewise at 16 and 24.  Gate/up: the B tile interleaves 32-row blocks of W1
-// and W3, so acc[i][2b] and acc[i][2b + 1] are the gate and up sums of the
-// same outputs; SiLU-and-multiply happens in registers and H is rounded to
-// bf16 once.  Loader waves write their 16-byte pieces to the staging area
+// Lane (r, q) = (lane % 16, lane / 16) holds columns 4 q + 0..3 of row r of
+// each 16 x 16 block.  For a pair of adjacent blocks (32 output columns) the
+// 16-lane rows of the wave swap (permlane16_swap: odd rows of the first
+// operand with even rows of the second) so that each lane holds 8 consecutive
+// columns: lane (r, q) gets columns 8 (q / 2) + 0..7 of block q % 2 of the
+// pair, one 16-byte piece.  Gate/up: the B tile interleaves 32-row blocks of
+// W1 and W3, so blocks 4p + {0, 1} and 4p + {2, 3} are the gate and up sums of
+// the same 32 outputs; SiLU-and-multiply happens in registers and H is
+// rounded to bf16 once.  Loader waves write their pieces to the staging area
 // (stage buffer 1), storer waves to the output; after a barrier the storers
 // also write the staged rows.  Storers never wait for their stores here.
 // Down GEMM with a combine plan (plan_dst != nullptr): a row whose plan entry
@@ -342,7 +339,7 @@ __device__ __forceinline__ u32x4 scale_chunk(const u32x4& v, float w) {
 // its accumulators, before staging) and written there, every other row to
 // the output.
 template <bool GUP>
-__device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16_t* __restrict__ out, int N_out,
+__device__ __forceinline__ void store_tile(const f32x4 (&acc)[kMI][kNJ], uint16_t* __restrict__ out, int N_out,
                                            int row0, int rows, int nt, int wave, int lane, uint8_t* staging,
                                            const int* plan_dst = nullptr, const float* plan_w = nullptr,
                                            uint16_t* __restrict__ parts = nullptr, int parts_rows = 0) {
@@ -351,11 +348,12 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
     constexpr int OUT_CH = OUT_RB / 16;               // 16-byte chunks per staged row
     constexpr int OUT_RPW = 256 / OUT_RB;             // staged rows per 256-byte bank window
     constexpr int STG_B = kWM * OUT_RB;               // staging bytes per loader wave
-    constexpr int NB = GUP ? kNJ / 2 : kNJ;           // 32-column output blocks of a wave
+    constexpr int NP = OUT_C / 32;                    // 32-column block pairs of a wave's output
     static_assert(kNL * STG_B <= kStageBytes, "staging fits in stage buffer 1");
     static_assert(OUT_RB == 128 || OUT_RB == 256, "staged row layout");
     // staged output rows: 16-byte chunk c of row r at physical chunk
-    // c ^ ((r / OUT_RPW) % OUT_CH), conflict-free for column writes and row reads
+    // c ^ ((r / OUT_RPW) % OUT_CH), conflict-free for column writes (8
+    // consecutive rows, one chunk) and row reads
     auto stg_swz = [](int r) { return (r / OUT_RPW) & (OUT_CH - 1); };
     const bool loader = wave < kNL;
     const int wm = wave / kWavesN, wn = wave % kWavesN;
@@ -363,13 +361,14 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
     // here, per tile, and not kept live across the K loop
     int ep_lane = lane;
     asm volatile("" : "+v"(ep_lane));
-    const int ep_row = ep_lane & 31, ep_half = ep_lane >> 5;
+    const int ep_row = ep_lane & 15, ep_q = ep_lane >> 4;
+    const int ep_c = 2 * (ep_q & 1) + (ep_q >> 1);     // this lane's chunk within a pair's four
     uint8_t* my_stg = staging + (loader ? wave : 0) * STG_B;
     const int out_c0 = (GUP ? nt * (kBN / 2) : nt * kBN) + wn * OUT_C;
 #pragma unroll
     for (int i = 0; i < kMI; ++i) {
-        if (!loader && wm * kWM + i * 32 >= rows) continue;            // wave-uniform
-        const int r = i * 32 + ep_row;                                 // row within the wave tile
+        if (!loader && wm * kWM + i * 16 >= rows) continue;            // wave-uniform
+        const int r = i * 16 + ep_row;                                 // row within the wave tile
         const bool row_ok = wm * kWM + r < rows;
         uint16_t* crow = out + static_cast<size_t>(row0 + wm * kWM + r) * N_out + out_c0;
         int dst = -1;
@@ -381,32 +380,32 @@ __device__ __forceinline__ void store_tile(const f32x16 (&acc)[kMI][kNJ], uint16
             else if (!loader) crow = parts + static_cast<size_t>(dst) * N_out + out_c0;
         }
 #pragma unroll
-        for (int jb = 0; jb < NB; ++jb) {
-            float v[16];
-            if constexpr (GUP) {
+        for (int pr = 0; pr < NP; ++pr) {
+            float v0[4], v1[4];                        // the pair's two output blocks
 #pragma unroll
-                for (int e = 0; e < 16; ++e) v[e] = silu(acc[i][2 * jb][e]) * acc[i][2 * jb + 1][e];
-            } else {
-#pragma unroll
-                for (int e = 0; e < 16; ++e) v[e] = acc[i][jb][e];
-            }
-#pragma unroll
-            for (int gp = 0; gp < 4; gp += 2) {
-                const uint32_t x0 = pack_bf16x2_rne(v[4 * gp + 0], v[4 * gp + 1]);
-                const uint32_t x1 = pack_bf16x2_rne(v[4 * gp + 2], v[4 * gp + 3]);
-                const uint32_t y0 = pack_bf16x2_rne(v[4 * gp + 4], v[4 * gp + 5]);
-                const uint32_t y1 = pack_bf16x2_rne(v[4 * gp + 6], v[4 * gp + 7]);
-                const auto ra = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-                const auto rb = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-                u32x4 o;
-                o[0] = ra[0]; o[1] = rb[0]; o[2] = ra[1]; o[3] = rb[1];
-                const int c = jb * 4 + gp + ep_half;                   // 8-column chunk in the wave tile
-                if (dst >= 0) o = scale_chunk(o, dw);
-                if (loader) {
-                    *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = o;
-                } else if (row_ok) {
-                    *reinterpret_cast<u32x4*>(crow + 8 * c) = o;
+            for (int e = 0; e < 4; ++e) {
+                if constexpr (GUP) {
+                    v0[e] = silu(acc[i][4 * pr + 0][e]) * acc[i][4 * pr + 2][e];
+                    v1[e] = silu(acc[i][4 * pr + 1][e]) * acc[i][4 * pr + 3][e];
+                } else {
+                    v0[e] = acc[i][2 * pr + 0][e];
+                    v1[e] = acc[i][2 * pr + 1][e];
                 }
+            }
+            const uint32_t x0 = pack_bf16x2_rne(v0[0], v0[1]);
+            const uint32_t x1 = pack_bf16x2_rne(v0[2], v0[3]);
+            const uint32_t y0 = pack_bf16x2_rne(v1[0], v1[1]);
+            const uint32_t y1 = pack_bf16x2_rne(v1[2], v1[3]);
+            const auto ra = __builtin_amdgcn_permlane16_swap(x0, y0, false, false);
+            const auto rb = __builtin_amdgcn_permlane16_swap(x1, y1, false, false);
+            u32x4 o;
+            o[0] = ra[0]; o[1] = rb[0]; o[2] = ra[1]; o[3] = rb[1];
+            const int c = 4 * pr + ep_c;                               // 8-column chunk in the wave tile
+            if (dst >= 0) o = scale_chunk(o, dw);
+            if (loader) {
+                *reinterpret_cast<u32x4*>(my_stg + r * OUT_RB + 16 * (c ^ stg_swz(r))) = o;
+            } else if (row_ok) {
+                *reinterpret_cast<u32x4*>(crow + 8 * c) = o;
             }
         }
     }
@@ -605,13 +604,13 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_gemm_bf16_kernel(
     int tile = worker_id();
     if (tile < total) start_tile(tile);
     while (tile < total) {
-        f32x16 acc[kMI][kNJ];
+        f32x4 acc[kMI][kNJ];
 #pragma unroll
         for (int i = 0; i < kMI; ++i)
 #pragma unroll
             for (int j = 0; j < kNJ; ++j)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+                for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
         k_loop(KT, lds, wm, wn, lm, wm * kWM < rows, acc, [&](int kt) {
             if (loader) wait_loads();              // this wave's part of stage kt has landed
@@ -827,13 +826,13 @@ __global__ __launch_bounds__(kNW * kWave, 1) void ffn_fused_bf16_kernel(
             issue(0);
         }
         while (t < Q) {
-            f32x16 acc[kMI][kNJ];
+            f32x4 acc[kMI][kNJ];
 #pragma unroll
             for (int i = 0; i < kMI; ++i)
 #pragma unroll
                 for (int j = 0; j < kNJ; ++j)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+                    for (int r = 0; r < 4; ++r) acc[i][j][r] = 0.0f;
 
             const int KT = T.KT;
             const bool ahead = KT >= 4;            // claim, publish and poll inside the K loop

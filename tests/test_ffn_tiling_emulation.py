@@ -45,7 +45,7 @@ STAGE_BYTES = (BM + BN) * ROW_B
 STAGES = 2
 WAVES_N = 2
 WM, WN = 64, 128
-MI = WM // 32
+MI, NJ = WM // 16, WN // 16          # 16 x 16 MFMA blocks per wave
 GROUP_M = 4
 N_XCC = 8
 SYNC_READY = 8 * 32 + 32
@@ -58,6 +58,10 @@ _PC = LANE & 7
 
 def _swz(r):
     return (r & 7) ^ ((r >> 3) & 1)
+
+
+FR_ROW, FR_Q = LANE & 15, LANE >> 4                  # fragment reads: row, 16-byte K chunk
+EP_C = 2 * ((LANE >> 4) & 1) + (LANE >> 5)          # epilogue: a lane's chunk within a pair's four
 
 
 COL_B = np.stack([(_PC ^ _swz(LD_ROW)) * 16, (_PC ^ _swz(ROWS_PER_LOAD + LD_ROW)) * 16]).astype(np.int64)
@@ -151,20 +155,19 @@ def check_loads(gu, l, row0, rows, nt, K, N_rows_b, a_rows_cap, gathered, row_sr
 
 def check_stores(gu, row0, rows, nt, N_out, out_rows_cap):
     OUT_C = WN // 2 if gu else WN
-    NB = (WN // 32) // 2 if gu else WN // 32
+    NP = OUT_C // 32
     for w in range(NW):
         wm, wn = w // WAVES_N, w % WAVES_N
         c0 = (nt * (BN // 2) if gu else nt * BN) + wn * OUT_C
         for i in range(MI):
-            r = wm * WM + i * 32 + (LANE & 31)
+            r = wm * WM + i * 16 + (LANE & 15)
             ok = r[None, :] < rows[:, None]
             grow = np.where(ok, row0[:, None] + r[None, :], 0)
             assert grow.max() < out_rows_cap
-            for jb in range(NB):
-                for gp in (0, 2):
-                    c = jb * 4 + gp + (LANE >> 5)
-                    col = c0[:, None] + 8 * c[None, :]
-                    assert col.min() >= 0 and col.max() + 8 <= N_out
+            for pr in range(NP):
+                c = 4 * pr + EP_C
+                col = c0[:, None] + 8 * c[None, :]
+                assert col.min() >= 0 and col.max() + 8 <= N_out
 
 
 def emulate_call(row_offsets, max_rows, d, inter, gathered=False, row_src=None, x_rows=0):
@@ -291,7 +294,7 @@ def test_combine_plan_indices_in_bounds():
     # own-row reads (storer waves) and staged-row reads (storer w reads loader w - NL's rows)
     for w in range(NW):
         wm = w // WAVES_N
-        r = np.arange(MI)[:, None] * 32 + (lane & 31)[None, :]
+        r = np.arange(MI)[:, None] * 16 + (lane & 15)[None, :]
         assert (wm * WM + r).min() >= 0 and (wm * WM + r).max() < BM
     for gu, out_rb in ((0, (WN) * 2),):
         rows_per_read = 1024 // out_rb
@@ -312,3 +315,86 @@ def test_combine_plan_indices_in_bounds():
                 for v in dst[used]:
                     assert 0 <= v < parts_rows
                     assert v * d + chunks.max() + 8 <= parts_rows * d
+
+
+def test_fragment_reads_inside_the_stage():
+    """k_step's LDS fragment reads (K steps 0 and 1 of either stage buffer):
+    every A read lies in the stage's A rows, every B read in its B rows, at a
+    16-byte chunk of the 128-byte row; the 16 lanes of one row group and chunk
+    hit 16 distinct bank windows of 16 bytes (8 consecutive rows: distinct
+    chunks; rows r and r + 8: chunks differ in the lowest bit)."""
+    for st in range(STAGES):
+        for ks in range(2):
+            pc = ((4 * ks + FR_Q) ^ _swz(FR_ROW)) * 16
+            assert pc.min() >= 0 and pc.max() + 16 <= ROW_B
+            for w in range(NW):
+                wm, wn = w // WAVES_N, w % WAVES_N
+                for i in range(MI):
+                    off = st * STAGE_BYTES + (wm * WM + i * 16 + FR_ROW) * ROW_B + pc
+                    assert off.min() >= st * STAGE_BYTES and off.max() + 16 <= st * STAGE_BYTES + BM * ROW_B
+                for j in range(NJ):
+                    off = st * STAGE_BYTES + (BM + wn * WN + j * 16 + FR_ROW) * ROW_B + pc
+                    assert off.min() >= st * STAGE_BYTES + BM * ROW_B
+                    assert off.max() + 16 <= (st + 1) * STAGE_BYTES
+            for q in range(4):
+                lanes = LANE[FR_Q == q]
+                for g in (lanes[:8], lanes[8:]):
+                    assert len(set((pc[g] // 16).tolist())) == 8
+                rows_pc = {(int(FR_ROW[l]) & 1, int(pc[l]) // 16) for l in lanes}
+                assert len(rows_pc) == 16
+
+
+def _permlane16_swap(x, y):
+    """v_permlane16_swap on 64-lane values: rows of 16 lanes; odd rows of the
+    first operand trade places with even rows of the second."""
+    x, y = x.copy(), y.copy()
+    for lo in (0, 32):
+        a, b = slice(lo + 16, lo + 32), slice(lo, lo + 16)
+        x[a], y[b] = y[b].copy(), x[a].copy()
+    return x, y
+
+
+@pytest.mark.parametrize("gu", [True, False])
+def test_epilogue_lane_layout_writes_each_output_once(gu):
+    """The epilogue's register-to-column map (store_tile): with the 16 x 16
+    MFMA output layout (lane (r, q) holds columns 4 q + 0..3 of row r of each
+    block, the weight fragment being the first operand), the permlane16_swap of
+    a block pair and the chunk index 4 pr + EP_C put every output column of
+    every row of the wave tile in exactly one 16-byte piece, at its own column;
+    for gate/up, each H column takes the gate from W1 block 4 pr + {0, 1} and
+    the up value from W3 block 4 pr + {2, 3} of the same B rows (the B tile
+    interleaves 32-row blocks of W1 and W3)."""
+    OUT_C = WN // 2 if gu else WN
+    NP = OUT_C // 32
+    r16, q = LANE & 15, LANE >> 4
+    # B-tile rows (wave-relative) that are W1 (gate) or W3 (up), and their H column
+    b_rows = np.arange(WN)
+    is_w3 = (b_rows // 32) % 2 == 1
+    h_col = (b_rows // 64) * 32 + b_rows % 32
+    seen = np.zeros((MI * 16, OUT_C), np.int64)
+    for i in range(MI):
+        for pr in range(NP):
+            pieces = []
+            for half in (0, 1):                     # packed pairs (e = 0, 1) and (e = 2, 3)
+                blocks = [4 * pr + 0, 4 * pr + 1] if gu else [2 * pr + 0, 2 * pr + 1]
+                # each packed value is tagged with the B row of its first element
+                x = 16 * blocks[0] + 4 * q + 2 * half
+                y = 16 * blocks[1] + 4 * q + 2 * half
+                pieces.append(_permlane16_swap(x, y))
+            (ra0, ra1), (rb0, rb1) = pieces
+            o = np.stack([ra0, rb0, ra1, rb1], 1)   # four packed pairs = 8 columns
+            c = 4 * pr + EP_C
+            for lane in range(64):
+                row = i * 16 + r16[lane]
+                for t in range(4):
+                    src = o[lane, t]
+                    for k in range(2):
+                        b = src + k
+                        col = 8 * c[lane] + 2 * t + k
+                        if gu:
+                            assert not is_w3[b] and h_col[b] == col
+                            assert is_w3[b + 32] and h_col[b + 32] == col    # its up partner block
+                        else:
+                            assert b == col
+                        seen[row, col] += 1
+    assert np.all(seen == 1)
