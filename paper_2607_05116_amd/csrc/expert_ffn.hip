@@ -212,7 +212,7 @@ struct LaneMap {
     int ld_row;          // direct loads: lane l writes row l / 8 of its 1 KiB block ...
     uint32_t col_b[2];   // ... at physical chunk l % 8, fetching logical chunk (l % 8) ^ swz(row):
                          // the swizzle of row (8 * blk + l / 8) is swz(l / 8) ^ (blk & 1)
-    int fr_row, fr_swz, fr_q;      // fragment reads: row r = ... + lane % 16, K quarter lane / 16
+    int fr_row, fr_swz, fr_kc;     // fragment reads: row r = ... + lane % 16, K chunk kc(lane / 16)
 };
 __device__ __forceinline__ LaneMap lane_map(int lane) {
     LaneMap m;
@@ -222,15 +222,18 @@ __device__ __forceinline__ LaneMap lane_map(int lane) {
     m.col_b[1] = static_cast<uint32_t>((pc ^ lds_swz(kRowsPerLoad + m.ld_row)) * 16);
     m.fr_row = lane & 15;
     m.fr_swz = lds_swz(m.fr_row);
-    m.fr_q = lane >> 4;
+    // K chunk of lane group g = lane / 16 within a K step: 0, 2, 1, 3, so
+    // that lanes l and l + 32 (read in one LDS pass) take chunks of opposite
+    // parity and, under the row swizzle, distinct banks
+    m.fr_kc = ((lane >> 3) & 2) | (lane >> 5);
     return m;
 }
 
 // Fragments and MFMAs.  One MFMA K step is K = 32 (two per stage).  Lane
-// (r, q) = (lane % 16, lane / 16) reads row r of each 16-row block at 16-byte
-// chunk 4 ks + q of K step ks (8 consecutive K; A and B take the same K
-// positions, so the contraction pairs them correctly whatever order the
-// hardware sums them in).  The MFMA takes the weight fragment as its first
+// (r, g) = (lane % 16, lane / 16) reads row r of each 16-row block at 16-byte
+// chunk 4 ks + kc(g) of K step ks, kc = (0, 2, 1, 3) (8 consecutive K; A and
+// B take the same K positions, so the contraction pairs them correctly
+// whatever order the hardware sums them in).  The MFMA takes the weight fragment as its first
 // operand, so a lane's 4 accumulators of block (i, j) hold output columns
 // 16 j + 4 q + 0..3 of tile row 16 i + r.
 __device__ __forceinline__ const bf16x8& frag_at(const uint8_t* p) { return *reinterpret_cast<const bf16x8*>(p); }
@@ -244,7 +247,7 @@ __device__ __forceinline__ const bf16x8& frag_at(const uint8_t* p) { return *rei
 __device__ __forceinline__ void k_step(const bf16x8 (&ac)[kMI], bf16x8 (&an)[kMI], bf16x8 (&b)[kNJ],
                                        f32x4 (&acc)[kMI][kNJ], const uint8_t* nst, int nks, int wm, int wn,
                                        const LaneMap& lm, bool rd) {
-    const int pc = ((4 * nks + lm.fr_q) ^ lm.fr_swz) << 4;
+    const int pc = ((4 * nks + lm.fr_kc) ^ lm.fr_swz) << 4;
     const uint8_t* sa = nst + (wm * kWM + lm.fr_row) * kRowB + pc;
     const uint8_t* sb = nst + (kBM + wn * kWN + lm.fr_row) * kRowB + pc;
 #pragma unroll
@@ -279,7 +282,7 @@ __device__ __forceinline__ void k_loop(int KT, const uint8_t* lds, int wm, int w
     bf16x8 a0[kMI], a1[kMI], b[kNJ];
     sync(0);
     if (active) {
-        const int pc = (lm.fr_q ^ lm.fr_swz) << 4;
+        const int pc = (lm.fr_kc ^ lm.fr_swz) << 4;
 #pragma unroll
         for (int i = 0; i < kMI; ++i) a0[i] = frag_at(lds + (wm * kWM + i * 16 + lm.fr_row) * kRowB + pc);
 #pragma unroll

@@ -60,7 +60,7 @@ def _swz(r):
     return (r & 7) ^ ((r >> 3) & 1)
 
 
-FR_ROW, FR_Q = LANE & 15, LANE >> 4                  # fragment reads: row, 16-byte K chunk
+FR_ROW, FR_KC = LANE & 15, ((LANE >> 3) & 2) | (LANE >> 5)   # fragment reads: row, 16-byte K chunk
 EP_C = 2 * ((LANE >> 4) & 1) + (LANE >> 5)          # epilogue: a lane's chunk within a pair's four
 
 
@@ -320,12 +320,18 @@ def test_combine_plan_indices_in_bounds():
 def test_fragment_reads_inside_the_stage():
     """k_step's LDS fragment reads (K steps 0 and 1 of either stage buffer):
     every A read lies in the stage's A rows, every B read in its B rows, at a
-    16-byte chunk of the 128-byte row; the 16 lanes of one row group and chunk
-    hit 16 distinct bank windows of 16 bytes (8 consecutive rows: distinct
-    chunks; rows r and r + 8: chunks differ in the lowest bit)."""
+    16-byte chunk of the 128-byte row; each lane group's 8 K values are one
+    chunk and the four groups cover the step's four chunks.  Banks (64 banks
+    of 4 bytes, a 256-byte window, two 128-byte rows): the 16 lanes of one
+    group, and lanes 8k .. 8k + 7 together with 8k + 32 .. 8k + 39 (the pairs
+    one pass of a 16-byte read serves), hit 16 distinct 16-byte bank slots."""
     for st in range(STAGES):
         for ks in range(2):
-            pc = ((4 * ks + FR_Q) ^ _swz(FR_ROW)) * 16
+            pc = ((4 * ks + FR_KC) ^ _swz(FR_ROW)) * 16
+            logical = (pc // 16) ^ _swz(FR_ROW)
+            for g in range(4):
+                assert len(set(logical[16 * g:16 * g + 16].tolist())) == 1
+            assert sorted(set(logical.tolist())) == list(range(4 * ks, 4 * ks + 4))
             assert pc.min() >= 0 and pc.max() + 16 <= ROW_B
             for w in range(NW):
                 wm, wn = w // WAVES_N, w % WAVES_N
@@ -336,12 +342,12 @@ def test_fragment_reads_inside_the_stage():
                     off = st * STAGE_BYTES + (BM + wn * WN + j * 16 + FR_ROW) * ROW_B + pc
                     assert off.min() >= st * STAGE_BYTES + BM * ROW_B
                     assert off.max() + 16 <= (st + 1) * STAGE_BYTES
-            for q in range(4):
-                lanes = LANE[FR_Q == q]
-                for g in (lanes[:8], lanes[8:]):
-                    assert len(set((pc[g] // 16).tolist())) == 8
-                rows_pc = {(int(FR_ROW[l]) & 1, int(pc[l]) // 16) for l in lanes}
-                assert len(rows_pc) == 16
+            slot = (FR_ROW & 1) * 8 + pc // 16            # 16-byte slot in the 256-byte window
+            for g in range(4):
+                assert len(set(slot[16 * g:16 * g + 16].tolist())) == 16
+            for k in range(4):
+                lanes = np.r_[8 * k:8 * k + 8, 8 * k + 32:8 * k + 40]
+                assert len(set(slot[lanes].tolist())) == 16
 
 
 def _permlane16_swap(x, y):
